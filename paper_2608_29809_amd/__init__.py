@@ -1,0 +1,8 @@
+"""Region-reuse DiT denoising step (RegionCache) on MI355X.
+
+The compute path is libregioncache.so: hand-written HIP kernels for gfx950
+behind the C ABI in include/regioncache.h.  `abi` binds that ABI with ctypes
+(argument marshalling only) and `runtime` adds device-memory plumbing with
+PyTorch.  Importing either without the built library raises ImportError.
+"""
+__all__ = ["abi", "runtime", "build"]

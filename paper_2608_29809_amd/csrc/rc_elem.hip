@@ -1,0 +1,304 @@
+// Row-wise and elementwise kernels of the step: active-row bookkeeping,
+// token gather + patch embedding, adaLN LayerNorm-modulate, timestep
+// conditioning GEMVs, the final layer fused with the DDIM update, and the
+// cache copies of the reuse path.
+#include "rc_common.h"
+#include "rc_elem.h"
+
+namespace rc {
+
+// rows[r] = (chain << 16) | token for r in [0, R); idx == null means the
+// dense identity set (token = r - offsets[chain]).
+__global__ void build_rows_kernel(const int *offsets, const int *idx, int B, int R, int *rows) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= R) return;
+  int b = 0;
+  while (b + 1 < B && offsets[b + 1] <= r) ++b;
+  const int tok = idx ? idx[r] : r - offsets[b];
+  rows[r] = (b << 16) | tok;
+}
+
+hipError_t launch_build_rows(const int *offsets, const int *idx, int B, int R, int *rows, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  hipLaunchKernelGGL(build_rows_kernel, dim3((R + 255) / 256), dim3(256), 0, s, offsets, idx, B, R, rows);
+  return hipGetLastError();
+}
+
+// Dense-step offsets: offsets[b] = b*N.
+__global__ void dense_offsets_kernel(int *offsets, int B, int N) {
+  const int b = threadIdx.x;
+  if (b <= B) offsets[b] = b * N;
+}
+
+hipError_t launch_dense_offsets(int *offsets, int B, int N, hipStream_t s) {
+  hipLaunchKernelGGL(dense_offsets_kernel, dim3(1), dim3(256), 0, s, offsets, B, N);
+  return hipGetLastError();
+}
+
+// X[r][:] = patch(token) . W_pe^T + b_pe + pos(token), or in token mode the
+// gathered hidden row.  One workgroup per row.
+template <typename T>
+__global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
+  const int r = blockIdx.x;
+  const int pk = a.rows[r];
+  const int b = row_chain(pk), tok = row_token(pk);
+  float *xrow = a.X + (size_t)r * a.C;
+  if (a.tokens_in) {
+    const T *src = (const T *)a.tokens_in + ((size_t)b * a.N + tok) * a.C;
+    for (int n = threadIdx.x; n < a.C; n += 256) xrow[n] = to_f<T>(src[n]);
+    return;
+  }
+  __shared__ float patch[16];
+  const int y = tok / a.gw, x = tok - (tok / a.gw) * a.gw;
+  if (threadIdx.x < 16) {
+    const int c = threadIdx.x >> 2, pi = (threadIdx.x >> 1) & 1, qi = threadIdx.x & 1;
+    const int Hl = a.gh * 2, Wl = a.gw * 2;
+    patch[threadIdx.x] = a.latent[(((size_t)b * 4 + c) * Hl + 2 * y + pi) * Wl + 2 * x + qi];
+  }
+  __syncthreads();
+  const T *W = (const T *)a.pe_w;
+  const int half = a.C / 2, quarter = a.C / 4;
+  const float log2_10000 = 13.287712379549449f;
+  for (int n = threadIdx.x; n < a.C; n += 256) {
+    float acc = a.pe_b[n];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) acc += to_f<T>(W[n * 16 + k]) * patch[k];
+    const int coord = n < half ? x : y;
+    const int kk = n % half;
+    const int f = kk % quarter;
+    const float w = exp2f(-(float)f / (float)quarter * log2_10000);
+    const float arg = (float)coord * w;
+    acc += kk < quarter ? sinf(arg) : cosf(arg);
+    xrow[n] = acc;
+  }
+}
+
+template <typename T> hipError_t launch_embed(const EmbedArgs &a, int R, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  hipLaunchKernelGGL(embed_kernel<T>, dim3(R), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+template hipError_t launch_embed<bf16>(const EmbedArgs &, int, hipStream_t);
+template hipError_t launch_embed<float>(const EmbedArgs &, int, hipStream_t);
+
+// out[r][:] = E( LN(X[r]) * (1 + scale) + shift ), scale/shift = table row + t0
+// row.  One wave per row; statistics in fp32 with a two-pass variance.
+template <typename T>
+__global__ __launch_bounds__(256) void ln_mod_kernel(const float *X, int R, int C, const float *table,
+                                                     const float *t0, int shift_row, float eps, T *out) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= R) return;
+  const float *x = X + (size_t)r * C;
+  constexpr int MAXV = 24;  // C <= 64*MAXV
+  float v[MAXV];
+  float s = 0.0f;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    const int n = lane + i * 64;
+    v[i] = n < C ? x[n] : 0.0f;
+    s += v[i];
+  }
+  const float mean = wave_sum(s) / C;
+  float q = 0.0f;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    const int n = lane + i * 64;
+    const float d = n < C ? v[i] - mean : 0.0f;
+    q += d * d;
+  }
+  const float rstd = rsqrtf(wave_sum(q) / C + eps);
+  const float *sh = table + (size_t)shift_row * C, *sc = sh + C;
+  const float *tsh = t0 + (size_t)shift_row * C, *tsc = tsh + C;
+  T *o = out + (size_t)r * C;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    const int n = lane + i * 64;
+    if (n < C) o[n] = from_f<T>((v[i] - mean) * rstd * (1.0f + sc[n] + tsc[n]) + sh[n] + tsh[n]);
+  }
+}
+
+template <typename T>
+hipError_t launch_ln_mod(const float *X, int R, int C, const float *table, const float *t0, int shift_row,
+                         float eps, void *out, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  if (C > 64 * 24) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(ln_mod_kernel<T>, dim3((R + 3) / 4), dim3(256), 0, s, X, R, C, table, t0, shift_row, eps,
+                     (T *)out);
+  return hipGetLastError();
+}
+template hipError_t launch_ln_mod<bf16>(const float *, int, int, const float *, const float *, int, float, void *, hipStream_t);
+template hipError_t launch_ln_mod<float>(const float *, int, int, const float *, const float *, int, float, void *, hipStream_t);
+
+// Timestep features e(t) = [cos(t f_k), sin(t f_k)], f_k = 10000^(-k/128).
+__global__ void timestep_features_kernel(float t, float *e) {
+  const int k = threadIdx.x;
+  if (k >= 128) return;
+  const float f = exp2f(-(float)k / 128.0f * 13.287712379549449f);
+  const float arg = t * f;
+  e[k] = cosf(arg);
+  e[128 + k] = sinf(arg);
+}
+
+hipError_t launch_timestep_features(float t, float *e, hipStream_t s) {
+  hipLaunchKernelGGL(timestep_features_kernel, dim3(1), dim3(128), 0, s, t, e);
+  return hipGetLastError();
+}
+
+// y[n] = act_out( W[n] . act_in(x) + b[n] ), one wave per output.
+template <typename T>
+__global__ __launch_bounds__(256) void gemv_kernel(const T *W, const float *bias, const float *x, int N, int K,
+                                                   int silu_in, int silu_out, float *y) {
+  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (n >= N) return;
+  const T *w = W + (size_t)n * K;
+  float acc = 0.0f;
+  for (int k = lane; k < K; k += 64) {
+    float xv = x[k];
+    if (silu_in) xv = silu(xv);
+    acc += to_f<T>(w[k]) * xv;
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) {
+    float v = acc + (bias ? bias[n] : 0.0f);
+    y[n] = silu_out ? silu(v) : v;
+  }
+}
+
+template <typename T>
+hipError_t launch_gemv(const void *W, const float *bias, const float *x, int N, int K, int silu_in, int silu_out,
+                       float *y, hipStream_t s) {
+  hipLaunchKernelGGL(gemv_kernel<T>, dim3((N + 3) / 4), dim3(256), 0, s, (const T *)W, bias, x, N, K, silu_in,
+                     silu_out, y);
+  return hipGetLastError();
+}
+template hipError_t launch_gemv<bf16>(const void *, const float *, const float *, int, int, int, int, float *, hipStream_t);
+template hipError_t launch_gemv<float>(const void *, const float *, const float *, int, int, int, int, float *, hipStream_t);
+
+// Final layer + DDIM for each computed row: eps = (LN(X)(1+sc)+sh) W_f^T + b_f
+// for the noise channels of the 2x2 patch, then x' = ca * x + cb * eps written
+// to the output latent and (if given) to the cached trajectory entry.
+template <typename T>
+__global__ __launch_bounds__(256) void final_ddim_kernel(FinalArgs a) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= a.R) return;
+  const int C = a.C;
+  const float *x = a.X + (size_t)r * C;
+  constexpr int MAXV = 24;
+  float v[MAXV];
+  float s = 0.0f;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    const int n = lane + i * 64;
+    v[i] = n < C ? x[n] : 0.0f;
+    s += v[i];
+  }
+  const float mean = wave_sum(s) / C;
+  float q = 0.0f;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    const int n = lane + i * 64;
+    const float d = n < C ? v[i] - mean : 0.0f;
+    q += d * d;
+  }
+  const float rstd = rsqrtf(wave_sum(q) / C + a.eps);
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    const int n = lane + i * 64;
+    if (n < C) {
+      const float sh = a.fin_sst[n] + a.t_emb[n];
+      const float sc = a.fin_sst[C + n] + a.t_emb[n];
+      v[i] = (v[i] - mean) * rstd * (1.0f + sc) + sh;
+    }
+  }
+  const int pk = a.rows[r];
+  const int b = row_chain(pk), tok = row_token(pk);
+  const int y = tok / a.gw, xx = tok - y * a.gw;
+  const int Hl = a.gh * 2, Wl = a.gw * 2;
+  const T *W = (const T *)a.fin_w;
+  for (int pix = 0; pix < 4; ++pix) {
+    const int pi = pix >> 1, qi = pix & 1;
+    for (int c = 0; c < 4; ++c) {
+      const int o = pix * a.out_ch + c;
+      float acc = 0.0f;
+#pragma unroll
+      for (int i = 0; i < MAXV; ++i) {
+        const int n = lane + i * 64;
+        if (n < C) acc += v[i] * to_f<T>(W[(size_t)o * C + n]);
+      }
+      acc = wave_sum(acc) + a.fin_b[o];
+      if (lane == 0) {
+        const size_t li = (((size_t)b * 4 + c) * Hl + 2 * y + pi) * Wl + 2 * xx + qi;
+        const float xn = a.ca * a.latent_in[li] + a.cb * acc;
+        a.latent_out[li] = xn;
+        if (a.traj_next) a.traj_next[b * a.traj_chain_stride + (li - (size_t)b * 4 * Hl * Wl)] = xn;
+      }
+    }
+  }
+}
+
+template <typename T> hipError_t launch_final_ddim(const FinalArgs &a, hipStream_t s) {
+  if (a.R <= 0) return hipSuccess;
+  if (a.C > 64 * 24) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(final_ddim_kernel<T>, dim3((a.R + 3) / 4), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+template hipError_t launch_final_ddim<bf16>(const FinalArgs &, hipStream_t);
+template hipError_t launch_final_ddim<float>(const FinalArgs &, hipStream_t);
+
+// Strided float copy of per-chain latents: dst[b] = src[b] (n floats each).
+__global__ void copy_chains_kernel(float *dst, long long dst_stride, const float *src, long long src_stride, int n,
+                                   int B) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (long)n * B) return;
+  const int b = i / n, k = i - (long)b * n;
+  dst[b * dst_stride + k] = src[b * src_stride + k];
+}
+
+hipError_t launch_copy_chains(float *dst, long long dst_stride, const float *src, long long src_stride, int n, int B,
+                              hipStream_t s) {
+  const long tot = (long)n * B;
+  if (tot <= 0) return hipSuccess;
+  hipLaunchKernelGGL(copy_chains_kernel, dim3((tot + 255) / 256), dim3(256), 0, s, dst, dst_stride, src, src_stride,
+                     n, B);
+  return hipGetLastError();
+}
+
+// H slot scatter: hslot(chain)[token][:] = src[r][:] for every active row,
+// 16-byte vectors; the chain of row r is found from the offsets.
+__global__ void scatter_rows_kernel(const int *offsets, const int *idx, int B, const V16 *src, int R,
+                                    int vec_per_row, V16 *hslot, long long chain_stride_vec) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (long)R * vec_per_row) return;
+  const int r = i / vec_per_row, c = i - (long)r * vec_per_row;
+  int b = 0;
+  while (b + 1 < B && offsets[b + 1] <= r) ++b;
+  hslot[b * chain_stride_vec + (long)idx[r] * vec_per_row + c] = src[i];
+}
+
+hipError_t launch_scatter_rows(const int *offsets, const int *idx, int B, const void *src, int R, int row_bytes,
+                               void *hslot, long long chain_stride_bytes, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  const int vpr = row_bytes / 16;
+  const long tot = (long)R * vpr;
+  hipLaunchKernelGGL(scatter_rows_kernel, dim3((tot + 255) / 256), dim3(256), 0, s, offsets, idx, B,
+                     (const V16 *)src, R, vpr, (V16 *)hslot, chain_stride_bytes / 16);
+  return hipGetLastError();
+}
+
+// Zero-fill with a kernel (no memset nodes in captured graphs).
+__global__ void zero_kernel(V16 *p, long n) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = V16{{0u, 0u, 0u, 0u}};
+}
+
+hipError_t launch_zero(void *p, size_t bytes, hipStream_t s) {
+  const long n = bytes / 16;
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(zero_kernel, dim3((n + 255) / 256), dim3(256), 0, s, (V16 *)p, n);
+  return hipGetLastError();
+}
+
+}  // namespace rc

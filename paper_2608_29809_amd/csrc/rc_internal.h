@@ -1,0 +1,76 @@
+// Internal launch interface between the C-ABI layer and the HIP kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace rc {
+
+enum GemmEpi {
+  EPI_STORE = 0,   // out = E(acc + bias)
+  EPI_GELU = 1,    // out = E(gelu_tanh(acc + bias))
+  EPI_RESID = 2,   // X += gate * (acc + bias); optional E copies of X (xt, H slot scatter, hidden rows)
+  EPI_QKV = 3,     // q -> out (compact), k -> K slot, v -> transposed V slot
+  EPI_TEXTKV = 4,  // text keys/values -> per-chain text K / transposed V
+};
+
+struct GemmArgs {
+  const void *A;  // [M][K] E, row stride lda
+  const void *W;  // [N][K] E
+  const float *bias;
+  int M, N, K, lda;
+  // EPI_STORE / EPI_GELU / EPI_QKV (queries)
+  void *out;
+  int ldo;
+  // EPI_RESID
+  float *X;
+  int ldx;
+  const float *gate;  // [N] or null (gate 1); the gate is gate[n] + gate2[n]
+  const float *gate2; // [N] or null
+  void *xt;           // [M][ldx] E copy of the updated X, or null
+  void *hrows;        // [M][N] E copy of the updated X (active hidden rows), or null
+  // scatter targets (EPI_RESID H slot, EPI_QKV K/V slots)
+  const int *rows;    // packed (chain<<16)|token per row
+  void *hslot;        // H of chain 0's slot, or null
+  void *kslot;        // K of chain 0's slot
+  void *vtslot;       // transposed V of chain 0's slot
+  long long chain_stride;  // elements between consecutive chains' slots
+  int tokens;              // N tokens per chain
+  int hidden;              // C
+  // EPI_TEXTKV
+  void *tkv;        // entry (layer, chain 0)
+  int text_len, text_pad;
+  long long tkv_chain_stride;
+};
+
+struct AttnArgs {
+  const void *Q;         // [R][C] E compact queries (chains concatenated)
+  const void *K;         // chain 0, head 0 keys [n_keys][72]
+  const void *Vt;        // chain 0, head 0 transposed values [72][n_keys]
+  long long chain_stride;  // elements between chains for K and Vt
+  long long head_stride;   // elements between heads (n_keys*72)
+  const int *offsets;    // [B+1] device row offsets of chains
+  int n_keys;            // keys per chain (multiple of 64)
+  int n_valid;           // keys >= n_valid are masked out
+  int hidden;            // C = heads*72
+  int splits;            // key-range splits (grid.y = heads*splits)
+  void *O;               // [R][C] E output (splits == 1)
+  float *Opart;          // [splits][R][C] unnormalised partial outputs (splits > 1)
+  float *ML;             // [splits][R][heads][2] running max (log2 domain) and sum
+  int total_rows;        // R (stride of the partial arrays)
+  // map emission (cross-attention)
+  int n_delta;
+  int delta[8];
+  float *pmaps;          // [heads][R][n_delta]
+  float scale_log2;      // log2(e)/sqrt(72)
+};
+
+template <typename T> hipError_t launch_gemm(const GemmArgs &a, int epi, hipStream_t s);
+template <typename T> hipError_t launch_attention(const AttnArgs &a, int n_chains, int max_rows,
+                                                  bool emit_maps, hipStream_t s);
+hipError_t launch_attn_combine(const float *Opart, const float *ML, void *O, bool bf16_out, int R,
+                               int heads, int splits, hipStream_t s);
+hipError_t launch_maps_reduce(const float *pmaps, const int *rows, float *maps, int R, int heads,
+                              int n_delta, int tokens, hipStream_t s);
+
+}  // namespace rc

@@ -128,10 +128,11 @@ def make_weights(s: ModelShape, seed: int = 0, std: float = 0.02,
     """Random-init weights ~N(0, std) for every matrix, bias and modulation
     table, stored as float32 holding bf16-exact values when `s.dtype` is bf16.
 
-    `stress=True` draws a "peaky" variant: the query/key projections are
-    scaled by 8 (sharp attention) and the gate rows of every modulation table
-    are shifted by +1 (gates near 1), so that attention and every gated branch
-    move the hidden state by O(1) rather than O(std)."""
+    `stress=True` draws a "peaky" variant: the self- and cross-attention query
+    and key projections are scaled by 3 (attention logits with a standard
+    deviation of about 4 instead of 0.5) and the gate rows of every modulation
+    table are shifted by +1 (gates near 1), so that attention and every gated
+    branch move the hidden state by O(1) rather than O(std)."""
     rng = _rng(seed, _S_WEIGHTS)
     C = s.hidden
     layers: List[Dict[str, np.ndarray]] = []
@@ -140,9 +141,9 @@ def make_weights(s: ModelShape, seed: int = 0, std: float = 0.02,
         for name, shp in layer_weight_shapes(s).items():
             a = rng.standard_normal(shp, dtype=np.float32) * np.float32(std)
             if stress and name == "qkv_w":
-                a[: 2 * C] *= 8.0
-            if stress and name == "xq_w":
-                a *= 8.0
+                a[: 2 * C] *= 3.0
+            if stress and name in ("xq_w", "xkv_w"):
+                a[:C] *= 3.0
             if stress and name == "sst":
                 a[2] += 1.0
                 a[5] += 1.0

@@ -1,0 +1,341 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle, and the
+method's invariants measured on the GPU.
+
+Tolerances: normwise relative error <= 2e-2 for bf16 storage and <= 1e-4 for
+fp32 storage against the float64 oracle; index lists bit-exact; derived masks
+equal except for tokens whose normalised score lies within 1e-3 of the
+threshold (and their dilation neighbourhoods)."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import synth
+from _cases import download_slot, oracle_text_kv, relerr, to_np, tol, upload_slot, weights
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from paper_2608_29809_amd.runtime import ActiveSet, RegionCacheModel, compact_mask, maps_from_logits
+
+
+def _say(*a):
+    print(*a, flush=True, file=sys.stderr)
+
+
+# --------------------------------------------------------------------------- index work (bit-exact)
+
+@pytest.mark.parametrize("B,N", [(1, 256), (3, 1024), (2, 4096)])
+def test_compact_bit_exact(B, N):
+    _say("compact", B, N)
+    rng = np.random.default_rng(N + B)
+    masks = (rng.random((B, N)) < rng.uniform(0.02, 0.6, size=(B, 1))).astype(np.uint8)
+    masks[0, :] = 0 if B > 1 else masks[0, :]
+    if B > 2:
+        masks[2, :] = 1
+    act = compact_mask(torch.from_numpy(masks).cuda())
+    torch.cuda.synchronize()
+    idx_ref, off_ref = O.compact(masks)
+    assert list(act.host) == off_ref.tolist()
+    assert np.array_equal(to_np(act.idx[:off_ref[-1]]).astype(np.int32), idx_ref)
+
+
+def _excused(scores, theta, gh, gw, band=1e-3):
+    near = (np.abs(scores - theta) < band).any(axis=1)
+    return O.dilate(near.reshape(gh, gw), 1).reshape(-1)
+
+
+def test_localize_maps_vs_oracle():
+    _say("localize maps")
+    s = synth.shape_c3()
+    gh, gw = s.grid_h, s.grid_w
+    B, nd = 3, 5
+    maps = np.stack([synth.planted_maps(gh * gw, nd, gh, gw, seed=b)[0] for b in range(B)])
+    maps[2] = np.random.default_rng(9).uniform(0, 1, maps[2].shape)  # no planted region
+    model = _tiny_model_for_grid(gh, gw)
+    mask, act = model.localize(torch.from_numpy(maps).cuda(), nd, 0.3, 1)
+    torch.cuda.synchronize()
+    mask = to_np(mask).astype(np.uint8)
+    for b in range(B):
+        m_ref, i_ref, sc = O.localize(maps[b], gh, gw, return_scores=True)
+        ok = (mask[b] == m_ref) | _excused(sc, 0.3, gh, gw)
+        assert ok.all(), b
+        g_idx = to_np(act.idx[act.host[b]:act.host[b + 1]]).astype(np.int32)
+        assert np.array_equal(g_idx, np.flatnonzero(mask[b]))
+        if not _excused(sc, 0.3, gh, gw).any():
+            assert np.array_equal(g_idx, i_ref)
+
+
+def _tiny_model_for_grid(gh, gw):
+    shp = synth.ModelShape(layers=1, grid_h=gh, grid_w=gw, dtype="bf16")
+    return RegionCacheModel(shp, synth.make_weights(shp, seed=0))
+
+
+def test_maps_from_logits_small():
+    _say("maps_from_logits small")
+    Z, delta, blob = synth.make_logits(2, 4, 256, 120, 16, 16, n_delta=4, seed=1)
+    g = maps_from_logits(torch.from_numpy(Z).cuda().to(torch.bfloat16), delta)
+    torch.cuda.synchronize()
+    ref = O.maps_from_logits(Z, delta)
+    assert relerr(to_np(g), ref) < 1e-5
+
+
+def test_localize_logits_full_size():
+    """The 1024 px localisation workload: logits [28, 16, 4096, 120] bf16 with
+    +3 on the delta columns over a blob -> mask + index list."""
+    _say("localize logits full")
+    s = synth.shape_c3()
+    gh, gw = s.grid_h, s.grid_w
+    Z, delta, blob = synth.make_logits(28, 16, gh * gw, 120, gh, gw, n_delta=6, seed=3, frac=0.12)
+    Zt = torch.from_numpy(Z).to(torch.bfloat16).cuda()
+    g = maps_from_logits(Zt, delta)
+    model = _tiny_model_for_grid(gh, gw)
+    mask, act = model.localize(g[None].contiguous(), len(delta), 0.3, 1)
+    torch.cuda.synchronize()
+    ref = O.maps_from_logits(Z, delta)
+    assert relerr(to_np(g), ref) < 1e-4
+    m_ref, i_ref, sc = O.localize(ref, gh, gw, n_avg=28 * 16, return_scores=True)
+    assert not _excused(sc, 0.3, gh, gw).any()
+    assert np.array_equal(to_np(mask[0]).astype(np.uint8), m_ref)
+    assert np.array_equal(to_np(act.idx[:act.total]).astype(np.int32), i_ref)
+    assert np.array_equal(m_ref.astype(bool), O.dilate(blob.reshape(gh, gw).astype(bool), 1).reshape(-1))
+
+
+# --------------------------------------------------------------------------- single fp32 block (token mode)
+
+@pytest.mark.parametrize("stress", [False, True])
+def test_c1_block_fp32(stress):
+    """One fp32 block over 256 tokens: dense build, then region reuse over the
+    4-aligned rectangle, each against the oracle at 1e-4."""
+    _say("c1 fp32 stress", stress)
+    case = synth.make_c1(0)
+    s = case["shape"]
+    W = synth.make_weights(s, seed=0, stress=stress) if stress else case["weights"]
+    model = RegionCacheModel(s, W)
+    cache = model.alloc_cache(1, 1)
+    tkv = model.prepare_text(model.to_storage(case["text"][None]))
+    tvec = torch.from_numpy(case["t_vec"]).cuda()
+    delta = case["delta"]
+    maps = torch.zeros((1, s.tokens, len(delta)), device="cuda")
+    model.build_cache(cache, 0, model.to_storage(case["x_prev"][None]), 0, -1, tkv, delta, maps, t_vec=tvec)
+    torch.cuda.synchronize()
+    Xd, Kd, Vd, md = O.dense_block_tokens(s, W, case["x_prev"], case["t_vec"], case["text"], delta)
+    got = download_slot(cache, 0, 1, 1)
+    assert relerr(got["H"][0, 0], Xd) < 1e-4
+    assert relerr(got["K"][0, 0], Kd) < 1e-4
+    assert relerr(got["V"][0, 0], Vd) < 1e-4
+    assert relerr(to_np(maps[0]), md) < 1e-4
+    # reuse over the rectangle, starting from the oracle's own dense cache
+    upload_slot(model, cache, 0, dict(K=Kd[None, None].astype(np.float32), V=Vd[None, None].astype(np.float32),
+                                      H=Xd[None, None].astype(np.float32)))
+    idx = np.flatnonzero(case["mask"])
+    act = ActiveSet.from_lists([idx])
+    maps.zero_()
+    model.reuse_step(cache, 0, act, model.to_storage(case["x_new"][None]), 0, -1, tkv, delta, maps, t_vec=tvec)
+    torch.cuda.synchronize()
+    Xr, Kr, Vr, Hr, mr = O.reuse_block_tokens(s, W, case["x_new"], idx, case["t_vec"], case["text"], Kd, Vd, Xd,
+                                              delta)
+    got = download_slot(cache, 0, 1, 1)
+    assert relerr(got["H"][0, 0], Hr) < 1e-4
+    assert relerr(got["K"][0, 0], Kr) < 1e-4
+    assert relerr(got["V"][0, 0], Vr) < 1e-4
+    # per-block delta of the active rows is also within tolerance
+    assert relerr(got["H"][0, 0][idx] - case["x_new"][idx], Hr[idx] - case["x_new"][idx]) < 1e-4
+    full_maps = np.zeros_like(md)
+    full_maps[idx] = mr
+    assert relerr(to_np(maps[0]), full_maps) < 1e-4
+    inactive = np.setdiff1d(np.arange(s.tokens), idx)
+    assert np.array_equal(got["H"][0, 0][inactive], Xd[inactive].astype(np.float32))
+
+
+# --------------------------------------------------------------------------- full-model steps (patch mode)
+
+def _reuse_case(shape, seed, per_chain_idx, t=500, t_next=450, stress=False, delta=(3, 17, 64), step=1,
+                steps=2, fuse=True):
+    W = weights(shape, seed, stress)
+    B = len(per_chain_idx)
+    txt = synth.make_text(shape, B, seed)
+    lat = synth.make_latent(shape, B, seed)
+    lat_next_cached = synth.make_latent(shape, B, seed, stream=77)
+    slot = synth.make_cache_slot(shape, B, seed)
+    model = RegionCacheModel(shape, W)
+    cache = model.alloc_cache(B, steps)
+    upload_slot(model, cache, step, slot)
+    for b in range(B):
+        cache.latent(b, step + 1).copy_(torch.from_numpy(lat_next_cached[b]))
+    tkv = model.prepare_text(model.to_storage(txt))
+    act = ActiveSet.from_lists(per_chain_idx)
+    maps = torch.zeros((B, shape.tokens, len(delta)), device="cuda")
+    lat_out = torch.empty(lat.shape, device="cuda")
+    lat_in = torch.from_numpy(lat).cuda()
+    hid = None
+    if not fuse:
+        hid = torch.empty((shape.layers, max(act.total, 1), shape.hidden), dtype=model.dtype, device="cuda")
+    model.reuse_step(cache, step, act, lat_in, t, t_next, tkv, list(delta), maps, lat_out, fuse=fuse,
+                     active_hidden=hid)
+    if not fuse:
+        model.update_cache(cache, step, act, hid)
+    torch.cuda.synchronize()
+    got = download_slot(cache, step, shape.layers, B)
+    got["latent_next"] = to_np(lat_out)
+    got["maps"] = to_np(maps)
+    got["traj_next"] = np.stack([to_np(cache.latent(b, step + 1)) for b in range(B)])
+    refs = []
+    for b in range(B):
+        tkv_o = oracle_text_kv(shape, W, txt[b])
+        cs = dict(K=slot["K"][:, b], V=slot["V"][:, b], H=slot["H"][:, b])
+        refs.append(O.reuse_step(shape, W, lat[b], t, t_next, tkv_o, per_chain_idx[b], cs, lat_next_cached[b],
+                                 np.array(delta)))
+    return got, refs, dict(slot=slot, lat_next_cached=lat_next_cached, model=model, cache=cache, W=W)
+
+
+def _check_reuse(shape, got, refs, per_chain_idx, ctx, tolerance=None):
+    tl = tolerance or tol(shape)
+    for b, r in enumerate(refs):
+        idx = np.asarray(per_chain_idx[b])
+        inact = np.setdiff1d(np.arange(shape.tokens), idx)
+        # inactive rows: the cache, bit for bit
+        assert np.array_equal(got["H"][:, b][:, inact], ctx["slot"]["H"][:, b][:, inact]), b
+        assert np.array_equal(got["K"][:, b][:, :, inact], ctx["slot"]["K"][:, b][:, :, inact]), b
+        assert np.array_equal(got["V"][:, b][:, :, inact], ctx["slot"]["V"][:, b][:, :, inact]), b
+        if idx.size == 0:
+            assert np.array_equal(got["latent_next"][b], ctx["lat_next_cached"][b])
+            continue
+        e_h = relerr(got["H"][:, b][:, idx], r["H"][:, idx])
+        e_k = relerr(got["K"][:, b][:, :, idx], r["K"][:, :, idx])
+        e_v = relerr(got["V"][:, b][:, :, idx], r["V"][:, :, idx])
+        e_l = relerr(got["latent_next"][b], r["latent_next"])
+        e_m = relerr(got["maps"][b], r["maps"])
+        _say(f"chain {b} R={idx.size}: H {e_h:.2e} K {e_k:.2e} V {e_v:.2e} latent {e_l:.2e} maps {e_m:.2e}")
+        assert e_h < tl and e_k < tl and e_v < tl and e_l < tl and e_m < tl
+        assert np.array_equal(got["traj_next"][b], got["latent_next"][b])
+        # inactive patches of the latent are the cached trajectory's
+        lp = O.latent_to_patches(got["latent_next"][b], 2)
+        cp = O.latent_to_patches(ctx["lat_next_cached"][b], 2)
+        assert np.array_equal(lp[inact], cp[inact])
+
+
+@pytest.mark.timeout(300)
+def test_c2_reuse_step_full_model():
+    """512 px, 28 blocks, bf16, t = 500, a 15 % rectangle (11 x 14 tokens)."""
+    _say("c2 reuse full")
+    s = synth.shape_c2()
+    idx = np.flatnonzero(synth.rect_mask(s.grid_h, s.grid_w, 11, 14, 9, 5))
+    got, refs, ctx = _reuse_case(s, 0, [idx])
+    _check_reuse(s, got, refs, [idx], ctx)
+
+
+@pytest.mark.parametrize("counts", [[1, 63, 0], [64, 65, 129], [127, 128, 1024]])
+def test_ragged_multichain_stress(counts):
+    """Several chains with unequal, ragged active counts (including 0 and N),
+    peaky weights so every block moves the state by O(1)."""
+    _say("ragged", counts)
+    s = synth.ModelShape(layers=2, grid_h=32, grid_w=32, dtype="bf16")
+    rng = np.random.default_rng(sum(counts))
+    per = [np.sort(rng.choice(s.tokens, size=c, replace=False)) for c in counts]
+    got, refs, ctx = _reuse_case(s, 5, per, stress=True, t=900, t_next=850)
+    _check_reuse(s, got, refs, per, ctx)
+
+
+def test_reuse_unfused_update_matches_fused():
+    s = synth.ModelShape(layers=2, grid_h=32, grid_w=32, dtype="bf16")
+    idx = [np.arange(100, 300)]
+    g1, _, _ = _reuse_case(s, 2, idx, fuse=True)
+    g2, _, _ = _reuse_case(s, 2, idx, fuse=False)
+    for k in ("H", "K", "V", "latent_next", "maps"):
+        assert np.array_equal(g1[k], g2[k]), k
+
+
+def test_dense_step_vs_oracle():
+    """Build-cache (dense) step: every token, 4 blocks at 1024 tokens, and the
+    all-active reuse step gives the same result bit for bit."""
+    _say("dense step")
+    s = synth.ModelShape(layers=4, grid_h=32, grid_w=32, dtype="bf16")
+    W = synth.make_weights(s, seed=4, stress=True)
+    txt = synth.make_text(s, 1, 4)
+    lat = synth.make_latent(s, 1, 4)
+    model = RegionCacheModel(s, W)
+    cache = model.alloc_cache(1, 3)
+    tkv = model.prepare_text(model.to_storage(txt))
+    delta = [0, 50, 119]
+    maps = torch.zeros((1, s.tokens, 3), device="cuda")
+    out = torch.empty(lat.shape, device="cuda")
+    model.build_cache(cache, 1, torch.from_numpy(lat).cuda(), 700, 650, tkv, delta, maps, out)
+    torch.cuda.synchronize()
+    got = download_slot(cache, 1, s.layers, 1)
+    ref = O.dense_step(s, W, lat[0], 700, 650, oracle_text_kv(s, W, txt[0]), np.array(delta))
+    for k in ("H", "K", "V"):
+        e = relerr(got[k][:, 0], ref[k])
+        _say(k, e)
+        assert e < 2e-2
+    assert relerr(to_np(out)[0], ref["latent_next"]) < 2e-2
+    assert relerr(to_np(maps)[0], ref["maps"]) < 2e-2
+    assert np.array_equal(to_np(cache.latent(0, 1)), lat[0])
+    assert np.array_equal(to_np(cache.latent(0, 2)), to_np(out)[0])
+    # all-active reuse == dense, bit for bit
+    cache2 = model.alloc_cache(1, 3)
+    cache2.buf.copy_(cache.buf)
+    maps2 = torch.zeros_like(maps)
+    out2 = torch.empty_like(out)
+    model.reuse_step(cache2, 1, ActiveSet.from_lists([np.arange(s.tokens)]), torch.from_numpy(lat).cuda(), 700,
+                     650, tkv, delta, maps2, out2)
+    torch.cuda.synchronize()
+    assert torch.equal(cache2.buf, cache.buf)
+    assert torch.equal(out2, out) and torch.equal(maps2, maps)
+
+
+def test_empty_mask_and_poison():
+    """No active token: slot unchanged and latent = cached trajectory.  Then
+    NaN in the stale cached rows of the active tokens never reaches an output."""
+    s = synth.ModelShape(layers=2, grid_h=32, grid_w=32, dtype="bf16")
+    W = synth.make_weights(s, seed=6)
+    txt = synth.make_text(s, 1, 6)
+    lat = synth.make_latent(s, 1, 6)
+    model = RegionCacheModel(s, W)
+    cache = model.alloc_cache(1, 2)
+    upload_slot(model, cache, 0, synth.make_cache_slot(s, 1, 6))
+    cache.latent(0, 1).copy_(torch.from_numpy(synth.make_latent(s, 1, 7)[0]))
+    before = cache.buf.clone()
+    tkv = model.prepare_text(model.to_storage(txt))
+    out = torch.empty(lat.shape, device="cuda")
+    model.reuse_step(cache, 0, ActiveSet.from_lists([np.zeros(0, np.int32)]), torch.from_numpy(lat).cuda(), 500,
+                     450, tkv, latent_out=out)
+    torch.cuda.synchronize()
+    assert torch.equal(cache.buf, before)
+    assert torch.equal(out[0], cache.latent(0, 1))
+    # poison
+    idx = np.arange(200, 260)
+    for l in range(s.layers):
+        cache.K(0, 0, l)[:, idx] = float("nan")
+        cache.Vt(0, 0, l)[:, :, idx] = float("nan")
+        cache.H(0, 0, l)[idx] = float("nan")
+    model.reuse_step(cache, 0, ActiveSet.from_lists([idx]), torch.from_numpy(lat).cuda(), 500, 450, tkv,
+                     latent_out=out)
+    torch.cuda.synchronize()
+    for l in range(s.layers):
+        assert torch.isfinite(cache.K(0, 0, l).float()).all()
+        assert torch.isfinite(cache.Vt(0, 0, l).float()).all()
+        assert torch.isfinite(cache.H(0, 0, l).float()).all()
+    assert torch.isfinite(out).all()
+
+
+def test_determinism():
+    s = synth.ModelShape(layers=2, grid_h=64, grid_w=64, dtype="bf16")
+    idx = [np.flatnonzero(synth.blob_mask(64, 64, 0.15, 2, np.random.default_rng(1)))]
+    g1, _, _ = _reuse_case(s, 8, idx)
+    g2, _, _ = _reuse_case(s, 8, idx)
+    for k in ("H", "K", "V", "latent_next", "maps"):
+        assert np.array_equal(g1[k], g2[k]), k
+
+
+@pytest.mark.timeout(400)
+def test_c3_reuse_step_full_size():
+    """1024 px (4096 tokens), 28 blocks, bf16, a 15 % blob mask, one reuse step
+    at the launch configuration the benchmark times."""
+    _say("c3 reuse full")
+    s = synth.shape_c3()
+    idx = np.flatnonzero(synth.blob_mask(64, 64, 0.15, 2, np.random.default_rng(0)))
+    got, refs, ctx = _reuse_case(s, 0, [idx], t=842, t_next=789)
+    _check_reuse(s, got, refs, [idx], ctx)
