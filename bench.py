@@ -1,0 +1,288 @@
+"""Benchmark of the region-reuse DiT denoising step on one MI355X.
+
+Workload: the 28-block PixArt-alpha-shaped model at 1024 px (latent
+4x128x128 -> 64x64 = 4096 tokens), bf16, a 20-step sampler schedule with
+timesteps linearly spaced 999 -> 0, and an edit mask of seeded elliptical
+blobs covering 10-20 % of the tokens.  Turn 0 fills the cache pool with 20
+dense steps; turn 1 (new prompt with edited tokens) runs 4 dense steps and 16
+region-reuse steps.  Everything is synthetic and seeded (random-init weights,
+N(0,1) text features and latents).
+
+One timed "step" is one region-reuse denoising step of turn 1 (gather + patch
+embedding, 28 blocks with the fused K/V scatter and the merge into the cached
+hidden state, final layer, DDIM update of the active patches).  The line also
+reports the dense step, the speedup of reuse over dense, and the whole 20-step
+editing turn (text preparation, 4 dense steps with map emission, edit-region
+localisation, 16 reuse steps) against an all-dense turn.
+
+Prints ONE JSON line.  `--gpus` above 1 is not supported (single-GPU build).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "DiT denoising steps/sec at 1024px, 10-20% active tokens; speedup vs dense"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=32)
+    ap.add_argument("--warmup", type=int, default=4)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--frac", type=float, default=None, help="active fraction (default: seeded in [0.10, 0.20])")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-layers", type=int, default=6, help="layers in the oracle timing sample")
+    ap.add_argument("--quick", action="store_true", help="skip the schedule legs (profiling runs)")
+    return ap.parse_args()
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: only --gpus 1 is supported; this build runs on one GPU (asked for {args.gpus})",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import synth
+    from paper_2608_29809_amd import abi
+    from paper_2608_29809_amd.runtime import ActiveSet, RegionCacheModel
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = "cuda"
+    shape = synth.shape_c3()
+    T = 20
+    n_dense = 4                        # floor(0.2 * 20) dense steps, the rest reuse
+    tgrid = synth.timestep_grid(T)
+    rng = np.random.default_rng([args.seed, 4242])
+    frac = args.frac if args.frac is not None else float(rng.uniform(0.10, 0.20))
+    n_blobs = int(rng.integers(1, 4))
+    mask = synth.blob_mask(shape.grid_h, shape.grid_w, frac, n_blobs, rng)
+    idx = np.flatnonzero(mask)
+    R = int(idx.size)
+    log(f"workload: 1024px, {shape.layers} blocks, N={shape.tokens}, R={R} ({R / shape.tokens:.1%}), blobs={n_blobs}")
+
+    t0 = time.time()
+    W = synth.make_weights(shape, seed=args.seed)
+    model = RegionCacheModel(shape, W)
+    cache = model.alloc_cache(1, T)
+    txt0 = synth.make_text(shape, 1, args.seed)
+    txt1, delta = synth.edit_text(shape, txt0, 5, args.seed)
+    noise = torch.from_numpy(synth.make_latent(shape, 1, args.seed)).to(dev)
+    tkv0 = model.prepare_text(model.to_storage(txt0))
+    lat = [torch.empty_like(noise) for _ in range(T + 1)]
+    lat[0].copy_(noise)
+    for s in range(T):  # turn 0: dense trajectory fills the cache pool
+        tn = int(tgrid[s + 1]) if s + 1 < T else -1
+        model.build_cache(cache, s, lat[s], int(tgrid[s]), tn, tkv0, latent_out=lat[s + 1])
+    torch.cuda.synchronize()
+    log(f"setup + turn 0 in {time.time() - t0:.1f}s")
+
+    act = ActiveSet.from_lists([idx])
+    tkv1 = model.prepare_text(model.to_storage(txt1))
+    maps = torch.zeros((1, shape.tokens, len(delta)), device=dev)
+    lat1 = [torch.empty_like(noise) for _ in range(T + 1)]
+    lat1[0].copy_(noise)
+    for s in range(n_dense):
+        model.build_cache(cache, s, lat1[s], int(tgrid[s]), int(tgrid[s + 1]), tkv1, delta,
+                          maps if s == n_dense - 1 else None, lat1[s + 1])
+    torch.cuda.synchronize()
+
+    reuse_steps = list(range(n_dense, T))
+
+    def reuse(k):
+        s = reuse_steps[k % len(reuse_steps)]
+        tn = int(tgrid[s + 1]) if s + 1 < T else -1
+        model.reuse_step(cache, s, act, lat1[s], int(tgrid[s]), tn, tkv1, latent_out=lat1[s + 1])
+
+    def dense(k):
+        s = reuse_steps[k % len(reuse_steps)]
+        tn = int(tgrid[s + 1]) if s + 1 < T else -1
+        model.build_cache(cache, s, lat1[s], int(tgrid[s]), tn, tkv1, latent_out=lat1[s + 1])
+
+    def time_loop(fn, steps, warmup):
+        for k in range(warmup):
+            fn(k)
+        torch.cuda.synchronize()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        w0 = time.perf_counter()
+        ev0.record()
+        for k in range(steps):
+            fn(k)
+        ev1.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - w0
+        return ev0.elapsed_time(ev1) / 1000.0, wall
+
+    # ---------------------------------------------------------------- headline: reuse steps
+    t_reuse, wall_reuse = time_loop(reuse, args.steps, args.warmup)
+    ms_reuse = 1000.0 * t_reuse / args.steps
+    log(f"reuse step: {ms_reuse:.3f} ms ({args.steps / t_reuse:.1f} steps/s; wall {wall_reuse:.3f}s)")
+
+    # ---------------------------------------------------------------- dense steps
+    n_d = max(4, args.steps // 4)
+    t_dense, _ = time_loop(dense, n_d, 2)
+    ms_dense = 1000.0 * t_dense / n_d
+    log(f"dense step: {ms_dense:.3f} ms")
+
+    # ---------------------------------------------------------------- per-kernel timing (HIP events)
+    model.set_kernel_timing(True)
+    n_prof = max(4, min(args.steps, 16))
+    for k in range(n_prof):
+        reuse(k)
+    torch.cuda.synchronize()
+    per = {}
+    for c, name in enumerate(abi.KERNEL_CLASSES):
+        ms, n = model.kernel_timing(c)
+        if n:
+            per[name] = dict(total_ms=ms / n_prof, launches=n // n_prof, avg_us=1000.0 * ms / n)
+    model.set_kernel_timing(False)
+    log("per-step kernel time by class: " + ", ".join(f"{k} {v['total_ms']:.3f}ms/{v['launches']}"
+                                                      for k, v in sorted(per.items(), key=lambda kv: -kv[1]['total_ms'])))
+
+    C, N, F, M = shape.hidden, shape.tokens, shape.mlp, shape.text_len
+    flops_per_launch = {  # algorithmic flops of one launch at R active rows (one chain)
+        "attn_self": 4.0 * R * N * C,
+        "attn_cross": 4.0 * R * M * C,
+        "gemm_qkv": 2.0 * R * 3 * C * C,
+        "gemm_fc1": 2.0 * R * F * C,
+        "gemm_fc2": 2.0 * R * C * F,
+        "gemm": 2.0 * R * C * C,
+    }
+    dom = max((k for k in per if k in flops_per_launch), key=lambda k: per[k]["total_ms"])
+    achieved = flops_per_launch[dom] / (per[dom]["avg_us"] * 1e-6) / 1e12
+    traffic = None
+    tpath = os.path.join(ROOT, "profiles", f"traffic_{dom}.json")
+    if os.path.exists(tpath):
+        try:
+            tj = json.load(open(tpath))
+            if tj.get("R") == R and tj.get("source_hash") == _kernel_hash(dom):
+                traffic = tj.get("bytes_per_launch")
+        except Exception:
+            traffic = None
+    roofline = dict(bound="mfma", kernel=dom, achieved=round(achieved, 2), peak=PEAK_BF16_TFLOPS,
+                    unit="TFLOP/s", frac=round(achieved / PEAK_BF16_TFLOPS, 4), traffic=traffic,
+                    flops_per_launch=flops_per_launch[dom], avg_launch_us=round(per[dom]["avg_us"], 3))
+
+    # ---------------------------------------------------------------- whole editing turn
+    schedule = None
+    if not args.quick:
+        def turn(all_dense: bool):
+            tk = model.prepare_text(model.to_storage(txt1))
+            mp = torch.zeros((1, shape.tokens, len(delta)), device=dev)
+            for s in range(T):
+                tn = int(tgrid[s + 1]) if s + 1 < T else -1
+                if all_dense or s < n_dense:
+                    model.build_cache(cache, s, lat1[s], int(tgrid[s]), tn, tk, delta,
+                                      mp if s == n_dense - 1 else None, lat1[s + 1])
+                    if s == n_dense - 1 and not all_dense:
+                        model.localize(mp, len(delta), 0.3, 1)  # the region read-out of Sec. 3.2
+                else:
+                    model.reuse_step(cache, s, act, lat1[s], int(tgrid[s]), tn, tk, latent_out=lat1[s + 1])
+
+        turn(False)
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        turn(False)
+        torch.cuda.synchronize()
+        t_turn = time.perf_counter() - w0
+        w0 = time.perf_counter()
+        turn(True)
+        torch.cuda.synchronize()
+        t_turn_dense = time.perf_counter() - w0
+        schedule = dict(turn_s=round(t_turn, 5), all_dense_turn_s=round(t_turn_dense, 5),
+                        steps_per_s=round(T / t_turn, 2), speedup_vs_all_dense=round(t_turn_dense / t_turn, 3),
+                        plan="4 dense (maps at step 3) + localisation + 16 reuse")
+        log(f"turn: {t_turn * 1000:.1f} ms vs all-dense {t_turn_dense * 1000:.1f} ms")
+
+    # ---------------------------------------------------------------- oracle on the host cores
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(shape, W, idx, args)
+
+    value = args.steps / t_reuse
+    out = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_reuse, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "1024px 28-block PixArt-alpha-shaped DiT, region-reuse denoising step",
+                   "tokens": N, "active_tokens": R, "active_frac": round(R / N, 4), "blobs": n_blobs,
+                   "batch": 1, "layers": shape.layers, "sampler_steps": T, "dense_steps": n_dense,
+                   "parallelism": "single GPU"},
+        "dense_step_ms": round(ms_dense, 4),
+        "dense_steps_per_s": round(1000.0 / ms_dense, 3),
+        "speedup_vs_dense": round(ms_dense / ms_reuse, 3),
+        "schedule": schedule,
+        "kernels_ms_per_step": {k: round(v["total_ms"], 4) for k, v in per.items()},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def _kernel_hash(cls):
+    import hashlib
+    f = {"attn_self": "rc_attn.hip", "attn_cross": "rc_attn.hip"}.get(cls, "rc_gemm.hip")
+    p = os.path.join(ROOT, "paper_2608_29809_amd", "csrc", f)
+    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+
+
+def cpu_baseline(shape, W, idx, args):
+    """The float64 oracle timed on this machine's host cores on a bounded
+    sample of the same reuse step: the first `--cpu-layers` blocks of the step
+    for one chain; the per-step time is scaled by layers/sampled-layers."""
+    import dataclasses
+    import oracle as O
+    import synth
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        threads = os.cpu_count()
+    Ls = max(1, min(args.cpu_layers, shape.layers))
+    sub = dataclasses.replace(shape, layers=Ls)
+    Wsub = dict(W)
+    Wsub["layers"] = W["layers"][:Ls]
+    txt = synth.make_text(shape, 1, args.seed)
+    lat = synth.make_latent(shape, 1, args.seed)
+    slot = synth.make_cache_slot(sub, 1, args.seed)
+    cache = dict(K=slot["K"][:, 0], V=slot["V"][:, 0], H=slot["H"][:, 0])
+    y = O.caption_projection(Wsub, txt[0])
+    tkv = [O.text_kv(lw, y, shape.heads) for lw in Wsub["layers"]]
+    w0 = time.perf_counter()
+    O.reuse_step(sub, Wsub, lat[0], 842, 789, tkv, idx, cache, lat[0])
+    dt = time.perf_counter() - w0
+    per_step = dt * shape.layers / Ls
+    log(f"oracle: {Ls} blocks in {dt:.2f}s -> {per_step:.2f}s per 28-block reuse step")
+    return dict(value=round(1.0 / per_step, 5), unit="steps/s", cores=int(threads), kind="oracle",
+                sample=f"one region-reuse step of one chain, first {Ls} of {shape.layers} blocks "
+                       f"(R={len(idx)} of {shape.tokens} tokens), float64 NumPy, time x {shape.layers}/{Ls}",
+                sample_seconds=round(dt, 3))
+
+
+if __name__ == "__main__":
+    main()

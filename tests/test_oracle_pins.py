@@ -485,3 +485,58 @@ def test_cosine_similarity():
     assert abs(O.cosine_similarity([1, 0], [0, 1])) < 1e-15
     assert abs(O.cosine_similarity([1, 2, 3], [2, 4, 6]) - 1) < 1e-15
     assert abs(O.cosine_similarity([1, 0], [1, 1]) - math.sqrt(0.5)) < 1e-15
+
+
+# --------------------------------------------------------------------------- projections against torch.nn modules
+
+def _linear(w, b):
+    m = torch.nn.Linear(w.shape[1], w.shape[0], dtype=torch.float64)
+    with torch.no_grad():
+        m.weight.copy_(torch.from_numpy(np.asarray(w, np.float64)))
+        m.bias.copy_(torch.from_numpy(np.asarray(b, np.float64)))
+    return m
+
+
+def test_caption_projection_matches_torch_mlp():
+    W = _tiny_weights(40)
+    txt = np.random.default_rng(40).standard_normal((TINY.text_len, TINY.text_dim))
+    mlp = torch.nn.Sequential(_linear(W["cap_w1"], W["cap_b1"]), torch.nn.GELU(approximate="tanh"),
+                              _linear(W["cap_w2"], W["cap_b2"]))
+    ref = mlp(torch.from_numpy(txt)).detach().numpy()
+    assert _rel(O.caption_projection(W, txt), ref) < 1e-13
+
+
+def test_timestep_embedding_and_adaln_match_torch():
+    W = _tiny_weights(41)
+    t = 613.0
+    e = torch.from_numpy(O.timestep_sinusoid(t))
+    mlp = torch.nn.Sequential(_linear(W["temb_w1"], W["temb_b1"]), torch.nn.SiLU(), _linear(W["temb_w2"], W["temb_b2"]))
+    temb_ref = mlp(e).detach().numpy()
+    temb = O.timestep_embedding(W, t)
+    assert _rel(temb, temb_ref) < 1e-13
+    blk = torch.nn.Sequential(torch.nn.SiLU(), _linear(W["tblock_w"], W["tblock_b"]))
+    t0_ref = blk(torch.from_numpy(temb_ref)).detach().numpy().reshape(6, -1)
+    assert _rel(O.adaln_single(W, temb), t0_ref) < 1e-13
+
+
+def test_text_kv_matches_torch_linear():
+    W = _tiny_weights(42)
+    lw = W["layers"][1]
+    y = np.random.default_rng(42).standard_normal((TINY.text_len, TINY.hidden))
+    kv = _linear(lw["xkv_w"], lw["xkv_b"])(torch.from_numpy(y)).detach()
+    k_ref, v_ref = kv.view(TINY.text_len, 2, TINY.heads, TINY.head_dim).unbind(1)
+    k, v = O.text_kv(lw, y, TINY.heads)
+    assert _rel(k, k_ref.numpy()) < 1e-13 and _rel(v, v_ref.numpy()) < 1e-13
+
+
+def test_final_layer_matches_torch():
+    W = _tiny_weights(43)
+    rng = np.random.default_rng(43)
+    X = rng.standard_normal((7, TINY.hidden)) * 2 + 0.5
+    temb = rng.standard_normal(TINY.hidden)
+    ln = torch.nn.LayerNorm(TINY.hidden, eps=1e-6, elementwise_affine=False, dtype=torch.float64)
+    sh = torch.from_numpy(W["fin_sst"][0].astype(np.float64) + temb)
+    sc = torch.from_numpy(W["fin_sst"][1].astype(np.float64) + temb)
+    h = ln(torch.from_numpy(X)) * (1 + sc) + sh
+    ref = _linear(W["fin_w"], W["fin_b"])(h).detach().numpy()
+    assert _rel(O.final_layer(W, X, temb), ref) < 1e-13
