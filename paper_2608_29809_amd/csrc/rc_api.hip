@@ -89,7 +89,8 @@ constexpr int kMaxSplits = 8;
 int part_cap_rows(int max_rows) { return kMaxSplits * std::min(max_rows, 1024); }
 
 struct WsLayout {
-  size_t rows, offsets, X, A1, Q, O, G, part, ml, pmaps, e, th, temb, t0, total;
+  size_t rows, offsets, X, A1, Q, O, G, part, ml, pmaps, e, th, temb, t0, gpart, total;
+  size_t gpart_floats;
   size_t txt_h, txt_y, txt_total;
 };
 
@@ -113,6 +114,8 @@ WsLayout ws_layout(const rc_ctx *c, int max_rows, int B) {
   w.th = take((size_t)c->C * 4);
   w.temb = take((size_t)c->C * 4);
   w.t0 = take((size_t)6 * c->C * 4);
+  w.gpart_floats = (size_t)std::min(max_rows, 2048) * 8 * c->C;
+  w.gpart = take(w.gpart_floats * 4);
   w.total = o;
   // text preparation reuses the front of the workspace
   size_t t = 0;
@@ -200,6 +203,18 @@ double alpha_bar(int t) {
 
 // ------------------------------------------------------------------ the step
 
+// One GEMM of the step: bf16 goes through the direct-to-LDS kernel with a
+// per-shape tile/split plan, fp32 through the register-staged kernel.
+template <typename T>
+rc_status gemm(rc_ctx *c, int cls, const rc::GemmArgs &g, int epi, float *part, size_t part_floats, hipStream_t s) {
+  if constexpr (sizeof(T) == 2) {
+    const rc::GemmPlan pl = rc::plan_gemm2(g.M, g.N, g.K, part ? part_floats : 0);
+    return timed(c, cls, s, [&] { return rc::launch_gemm2(g, epi, pl, part, s); });
+  } else {
+    return timed(c, cls, s, [&] { return rc::launch_gemm<T>(g, epi, s); });
+  }
+}
+
 template <typename T>
 rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_step_io *io, bool dense,
                    const rc_active_set *act, void *active_hidden, bool fuse, void *ws, size_t ws_bytes,
@@ -250,6 +265,8 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
   float *part = (float *)(wsb + wl.part), *ml = (float *)(wsb + wl.ml), *pmaps = (float *)(wsb + wl.pmaps);
   float *e = (float *)(wsb + wl.e), *th = (float *)(wsb + wl.th), *temb = (float *)(wsb + wl.temb);
   float *t0 = (float *)(wsb + wl.t0);
+  float *gpart = (float *)(wsb + wl.gpart);
+  const size_t gpf = wl.gpart_floats;
 
   if (dense) RC_TRY(timed(c, RC_KC_MISC, s, [&] { return rc::launch_dense_offsets((int *)offsets_dev, B, N, s); }));
   RC_TRY(timed(c, RC_KC_MISC, s, [&] {
@@ -290,13 +307,25 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
     RC_TRY(timed(c, RC_KC_EMBED, s, [&] { return rc::launch_embed<T>(ea, R, s); }));
   }
 
-  // self-attention key splits: enough workgroups to fill the chip
+  // self-attention key splits: fill 3 workgroups x 256 CUs with as few
+  // splits as possible (the bf16 kernel takes uneven splits)
   long qtiles = 0;
   for (int b = 0; b < B; ++b) qtiles += (counts[b] + 127) / 128;
   int splits = 1;
-  while (splits < kMaxSplits && qtiles * H * splits < 512 && N % (64 * splits * 2) == 0 &&
-         (long)R * splits * 2 <= part_cap_rows(R))
-    splits *= 2;
+  if (sizeof(T) == 2) {
+    double best = -1.0;
+    const int max_s = std::min(N / 64, 16);
+    for (int sp = 1; sp <= max_s; ++sp) {
+      if ((long)R * sp > part_cap_rows(R) && sp > 1) break;
+      const long wgs = qtiles * H * sp;
+      const double eff = wgs / (std::ceil(wgs / 768.0) * 768.0) - 0.01 * sp;  // 3 workgroups per CU
+      if (eff > best) { best = eff; splits = sp; }
+    }
+  } else {
+    while (splits < kMaxSplits && qtiles * H * splits < 512 && N % (64 * splits * 2) == 0 &&
+           (long)R * splits * 2 <= part_cap_rows(R))
+      splits *= 2;
+  }
 
   const bool emit = io->maps && io->n_delta > 0;
   const long long slot_chain_stride = (long long)T_ * L * slot_elems(c);
@@ -314,14 +343,17 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       g.A = A1; g.W = lw.qkv_w; g.bias = lw.qkv_b; g.M = R; g.N = 3 * C; g.K = C; g.lda = C;
       g.out = Q; g.ldo = C; g.rows = rows; g.kslot = Ks; g.vtslot = Vts;
       g.chain_stride = slot_chain_stride; g.tokens = N; g.hidden = C;
-      RC_TRY(timed(c, RC_KC_GEMM_QKV, s, [&] { return rc::launch_gemm<T>(g, rc::EPI_QKV, s); }));
+      RC_TRY(gemm<T>(c, RC_KC_GEMM_QKV, g, rc::EPI_QKV, gpart, gpf, s));
     }
     {  // region-level sparse self-attention over the whole slot
       rc::AttnArgs a{};
       a.Q = Q; a.K = Ks; a.Vt = Vts; a.chain_stride = slot_chain_stride; a.head_stride = (long long)N * rc::kHeadDim;
       a.offsets = offsets_dev; a.n_keys = N; a.n_valid = N; a.hidden = C; a.splits = splits;
       a.O = O; a.Opart = part; a.ML = ml; a.total_rows = R; a.scale_log2 = scale_log2;
-      RC_TRY(timed(c, RC_KC_ATTN_SELF, s, [&] { return rc::launch_attention<T>(a, B, max_rb, false, s); }));
+      RC_TRY(timed(c, RC_KC_ATTN_SELF, s, [&] {
+        return sizeof(T) == 2 ? rc::launch_attention2(a, B, max_rb, false, s)
+                              : rc::launch_attention<T>(a, B, max_rb, false, s);
+      }));
       if (splits > 1)
         RC_TRY(timed(c, RC_KC_ATTN_COMBINE, s, [&] {
           return rc::launch_attn_combine(part, ml, O, sizeof(T) == 2, R, H, splits, s);
@@ -331,12 +363,12 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       rc::GemmArgs g{};
       g.A = O; g.W = lw.proj_w; g.bias = lw.proj_b; g.M = R; g.N = C; g.K = C; g.lda = C;
       g.X = X; g.ldx = C; g.gate = lw.sst + 2 * C; g.gate2 = t0 + 2 * C; g.xt = A1;
-      RC_TRY(timed(c, RC_KC_GEMM, s, [&] { return rc::launch_gemm<T>(g, rc::EPI_RESID, s); }));
+      RC_TRY(gemm<T>(c, RC_KC_GEMM, g, rc::EPI_RESID, gpart, gpf, s));
     }
     {  // cross-attention query
       rc::GemmArgs g{};
       g.A = A1; g.W = lw.xq_w; g.bias = lw.xq_b; g.M = R; g.N = C; g.K = C; g.lda = C; g.out = Q; g.ldo = C;
-      RC_TRY(timed(c, RC_KC_GEMM, s, [&] { return rc::launch_gemm<T>(g, rc::EPI_STORE, s); }));
+      RC_TRY(gemm<T>(c, RC_KC_GEMM, g, rc::EPI_STORE, gpart, gpf, s));
     }
     {  // cross-attention to the text, emitting the delta-token maps
       const T *tkv = (const T *)io->text_kv + (size_t)l * B * text_kv_elems_per_entry(c);
@@ -350,7 +382,10 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
         for (int j = 0; j < io->n_delta; ++j) a.delta[j] = io->delta_cols_host[j];
         a.pmaps = pmaps;
       }
-      RC_TRY(timed(c, RC_KC_ATTN_CROSS, s, [&] { return rc::launch_attention<T>(a, B, max_rb, emit, s); }));
+      RC_TRY(timed(c, RC_KC_ATTN_CROSS, s, [&] {
+        return sizeof(T) == 2 ? rc::launch_attention2(a, B, max_rb, true, s)
+                              : rc::launch_attention<T>(a, B, max_rb, emit, s);
+      }));
       if (emit)
         RC_TRY(timed(c, RC_KC_MISC, s, [&] {
           return rc::launch_maps_reduce(pmaps, rows, io->maps, R, H, io->n_delta, N, s);
@@ -360,13 +395,13 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       rc::GemmArgs g{};
       g.A = O; g.W = lw.xproj_w; g.bias = lw.xproj_b; g.M = R; g.N = C; g.K = C; g.lda = C;
       g.X = X; g.ldx = C;
-      RC_TRY(timed(c, RC_KC_GEMM, s, [&] { return rc::launch_gemm<T>(g, rc::EPI_RESID, s); }));
+      RC_TRY(gemm<T>(c, RC_KC_GEMM, g, rc::EPI_RESID, gpart, gpf, s));
     }
     RC_TRY(timed(c, RC_KC_NORM, s, [&] { return rc::launch_ln_mod<T>(X, R, C, lw.sst, t0, 3, c->cfg.ln_eps, A1, s); }));
     {  // MLP up + GELU
       rc::GemmArgs g{};
       g.A = A1; g.W = lw.fc1_w; g.bias = lw.fc1_b; g.M = R; g.N = F; g.K = C; g.lda = C; g.out = G; g.ldo = F;
-      RC_TRY(timed(c, RC_KC_GEMM_FC1, s, [&] { return rc::launch_gemm<T>(g, rc::EPI_GELU, s); }));
+      RC_TRY(gemm<T>(c, RC_KC_GEMM_FC1, g, rc::EPI_GELU, gpart, gpf, s));
     }
     {  // MLP down + gate + residual; merge into the cached hidden state
       rc::GemmArgs g{};
@@ -375,7 +410,7 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       g.rows = rows; g.hidden = C; g.chain_stride = slot_chain_stride;
       if (dense || fuse) g.hslot = Hs;
       else g.hrows = (T *)active_hidden + (size_t)l * R * C;
-      RC_TRY(timed(c, RC_KC_GEMM_FC2, s, [&] { return rc::launch_gemm<T>(g, rc::EPI_RESID, s); }));
+      RC_TRY(gemm<T>(c, RC_KC_GEMM_FC2, g, rc::EPI_RESID, gpart, gpf, s));
     }
   }
 
@@ -418,11 +453,11 @@ rc_status run_text(rc_ctx *c, const void *txt, int B, void *text_kv, void *ws, s
     rc::GemmArgs g{};
     g.A = txt; g.W = c->w.cap_w1; g.bias = c->w.cap_b1; g.M = B * M; g.N = C; g.K = c->cfg.text_dim;
     g.lda = c->cfg.text_dim; g.out = wsb + wl.txt_h; g.ldo = C;
-    RC_TRY(timed(c, RC_KC_GEMM, s, [&] { return rc::launch_gemm<T>(g, rc::EPI_GELU, s); }));
+    RC_TRY(gemm<T>(c, RC_KC_GEMM, g, rc::EPI_GELU, nullptr, 0, s));
     rc::GemmArgs g2{};
     g2.A = wsb + wl.txt_h; g2.W = c->w.cap_w2; g2.bias = c->w.cap_b2; g2.M = B * M; g2.N = C; g2.K = C;
     g2.lda = C; g2.out = wsb + wl.txt_y; g2.ldo = C;
-    RC_TRY(timed(c, RC_KC_GEMM, s, [&] { return rc::launch_gemm<T>(g2, rc::EPI_STORE, s); }));
+    RC_TRY(gemm<T>(c, RC_KC_GEMM, g2, rc::EPI_STORE, nullptr, 0, s));
     y = wsb + wl.txt_y;
   }
   for (int l = 0; l < c->L; ++l) {
@@ -430,7 +465,7 @@ rc_status run_text(rc_ctx *c, const void *txt, int B, void *text_kv, void *ws, s
     g.A = y; g.W = c->layers[l].xkv_w; g.bias = c->layers[l].xkv_b; g.M = B * M; g.N = 2 * C; g.K = C; g.lda = C;
     g.tkv = (T *)text_kv + (size_t)l * B * text_kv_elems_per_entry(c);
     g.text_len = M; g.text_pad = c->Mp; g.tkv_chain_stride = (long long)text_kv_elems_per_entry(c); g.hidden = C;
-    RC_TRY(timed(c, RC_KC_GEMM, s, [&] { return rc::launch_gemm<T>(g, rc::EPI_TEXTKV, s); }));
+    RC_TRY(gemm<T>(c, RC_KC_GEMM, g, rc::EPI_TEXTKV, nullptr, 0, s));
   }
   return RC_OK;
 }

@@ -1,0 +1,253 @@
+// bf16 variable-query-length attention, second form (head dim 72).
+//
+// Same decomposition as rc_attn.hip -- one workgroup = 4 waves = 128 queries
+// of one (chain, head, key range), each wave 32 queries, scores formed
+// transposed (S^T = K Q^T) so each lane owns one query, probabilities reused
+// in registers as the B operand of O^T = V^T P^T -- with these changes:
+//
+// * K and V^T tiles (64 keys) move global -> LDS with global_load_lds_dwordx4
+//   into a two-stage ring, one barrier per tile.
+// * Key order inside a 32-key sub-tile: the K row that lane m supplies is
+//   key pi(m) = ((m>>4)&1)*16 + ((m>>2)&1)*8 + ((m>>3)&1)*4 + (m&3).  Then the
+//   16 accumulators of lane group g are keys c*16 + g*8 + k (c = 0,1; k = 0..7)
+//   in order, so each PV instruction reads 8 contiguous keys of V^T (one
+//   16-byte LDS read), and the eight lanes of every 16-byte read phase of the
+//   K tile (row stride 144 bytes) touch eight disjoint bank groups.
+// * V^T tile rows are 128 bytes with their 16-byte chunks XOR-swizzled by
+//   (row & 7), conflict-free for the 32-row operand reads.
+// * Softmax in the exp2 domain on raw scores: p = exp2(s*c - m*c) (one FMA +
+//   v_exp), running max on raw scores, and the output rescale is skipped when
+//   no query of the wave raised its maximum.
+// * Key ranges split unevenly over grid.y so the grid fills the chip; the
+//   deterministic combine is rc_attn.hip's.
+#include "rc_common.h"
+#include "rc_internal.h"
+
+namespace rc {
+
+constexpr int A2_BQ = 128, A2_BK = 64;
+
+__device__ __forceinline__ int key_perm2(int m) {
+  return ((m >> 4) & 1) * 16 + ((m >> 2) & 1) * 8 + ((m >> 3) & 1) * 4 + (m & 3);
+}
+
+__device__ __forceinline__ void lds_barrier2() { asm volatile("s_barrier" ::: "memory"); }
+__device__ __forceinline__ void wait_vm0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+template <bool CROSS>
+__global__ __launch_bounds__(256, 2) void attn2_kernel(AttnArgs a) {
+  constexpr int D = kHeadDim;
+  constexpr int KT_BYTES = A2_BK * D * 2;      // 9216: K tile [64][72]
+  constexpr int VT_BYTES = D * A2_BK * 2;      // 9216: V^T tile [72][64]
+  constexpr int STAGE = KT_BYTES + VT_BYTES;
+  constexpr int K_CH = KT_BYTES / 16;          // 576 chunks
+  __shared__ __attribute__((aligned(1024))) char lds[2 * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5, r32 = lane & 31;
+  const int heads = a.hidden / D;
+  const int b = blockIdx.z;
+  const int h = blockIdx.y % heads, split = blockIdx.y / heads;
+  const int r0 = a.offsets[b], r1 = a.offsets[b + 1];
+  const int q0 = r0 + blockIdx.x * A2_BQ;
+  if (q0 >= r1) return;  // uniform across the workgroup
+  const int my_q = q0 + wave * 32 + r32;
+  const bool q_ok = my_q < r1;
+
+  const int n_tiles = a.n_keys / A2_BK;
+  const int t_beg = (int)((long)split * n_tiles / a.splits), t_end = (int)((long)(split + 1) * n_tiles / a.splits);
+  const bf16 *Kg = (const bf16 *)a.K + b * a.chain_stride + h * a.head_stride;
+  const bf16 *Vg = (const bf16 *)a.Vt + b * a.chain_stride + h * a.head_stride;
+
+  bf16x8 qf[5];
+  {
+    const bf16 *qrow = (const bf16 *)a.Q + (size_t)(q_ok ? my_q : q0) * a.hidden + h * D;
+#pragma unroll
+    for (int c = 0; c < 5; ++c) {
+      const int d0 = c * 16 + g * 8;
+      qf[c] = Mfma<bf16>::zero();
+      if (q_ok && d0 < D) qf[c] = *(const bf16x8 *)(qrow + d0);
+    }
+  }
+
+  auto issue = [&](int stage, int tile) {
+    char *ks = lds + stage * STAGE, *vs = ks + KT_BYTES;
+    const int key0 = tile * A2_BK;
+    const char *kt = (const char *)(Kg + (size_t)key0 * D);
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+      const int base = i * 256 + wave * 64;
+      if (base < K_CH)
+        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)(kt + (base + lane) * 16),
+                                         (__attribute__((address_space(3))) void *)(ks + base * 16), 16, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+      const int base = i * 256 + wave * 64;
+      if (base < K_CH) {
+        const int ch = base + lane, d = ch >> 3, lc = (ch & 7) ^ (d & 7);
+        const bf16 *src = Vg + (size_t)d * a.n_keys + key0 + lc * 8;
+        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
+                                         (__attribute__((address_space(3))) void *)(vs + base * 16), 16, 0, 0);
+      }
+    }
+  };
+
+  f32x16 o[3];
+#pragma unroll
+  for (int t = 0; t < 3; ++t)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) o[t][e] = 0.0f;
+  float m_run = -INFINITY, l_run = 0.0f;
+  float sd[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) sd[j] = -INFINITY;
+  const float c2 = a.scale_log2;
+
+  if (t_beg < t_end) issue(0, t_beg);
+  for (int tile = t_beg; tile < t_end; ++tile) {
+    const int stage = (tile - t_beg) & 1;
+    wait_vm0();
+    lds_barrier2();
+    if (tile + 1 < t_end) issue(stage ^ 1, tile + 1);
+    const char *ks = lds + stage * STAGE, *vs = ks + KT_BYTES;
+    const int key0 = tile * A2_BK;
+
+    f32x16 s[2];
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) s[st][e] = 0.0f;
+      const char *krow = ks + (st * 32 + key_perm2(r32)) * (D * 2);
+#pragma unroll
+      for (int c = 0; c < 5; ++c) {
+        const int d0 = c * 16 + g * 8;
+        bf16x8 kf = Mfma<bf16>::zero();
+        if (d0 < D) kf = *(const bf16x8 *)(krow + d0 * 2);
+        s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], s[st], 0, 0, 0);
+      }
+    }
+
+    // lane group g, sub-tile st, accumulator e = c*8 + k  <->  key st*32 + c*16 + g*8 + k
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        if (CROSS) {
+          const int key = key0 + st * 32 + (e >> 3) * 16 + g * 8 + (e & 7);
+          if (key >= a.n_valid) s[st][e] = -INFINITY;
+        }
+        tmax = fmaxf(tmax, s[st][e]);
+      }
+    if (CROSS) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (j < a.n_delta) {
+          const int rel = a.delta[j] - key0;
+          if (rel >= 0 && rel < A2_BK && ((rel >> 3) & 1) == g) {
+            const int st = rel >> 5, e = ((rel >> 4) & 1) * 8 + (rel & 7);
+#pragma unroll
+            for (int ee = 0; ee < 16; ++ee)
+              if (ee == e) sd[j] = st ? s[1][ee] : s[0][ee];
+          }
+        }
+      }
+    }
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    const float m_new = fmaxf(m_run, tmax);
+    if (__any(m_new > m_run)) {
+      const float alpha = (m_run == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m_run - m_new) * c2);
+      l_run *= alpha;
+#pragma unroll
+      for (int t = 0; t < 3; ++t)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[t][e] *= alpha;
+      m_run = m_new;
+    }
+    const float mc = (m_run == -INFINITY) ? 0.0f : m_run * c2;
+    bf16x8 pf[2][2];
+    float psum = 0.0f;
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][c * 8 + k], c2, -mc));
+          psum += p;
+          pf[st][c][k] = (bf16)p;
+        }
+    l_run += psum;
+
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const int lc = st * 4 + c * 2 + g;  // logical 16-byte chunk of the 64-key row
+#pragma unroll
+        for (int t = 0; t < 3; ++t) {
+          const int d = t * 32 + r32;
+          bf16x8 vf = Mfma<bf16>::zero();
+          if (d < D) vf = *(const bf16x8 *)(vs + d * 128 + ((lc ^ (d & 7)) << 4));
+          o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[st][c], o[t], 0, 0, 0);
+        }
+      }
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  if (CROSS && a.pmaps) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (j < a.n_delta) {
+        const int owner = (a.delta[j] >> 3) & 1;
+        float p = (g == owner && m_run != -INFINITY) ? __builtin_amdgcn_exp2f((sd[j] - m_run) * c2) / l_tot : 0.0f;
+        p += __shfl_xor(p, 32, 64);
+        if (g == 0 && q_ok) a.pmaps[((size_t)h * a.total_rows + my_q) * a.n_delta + j] = p;
+      }
+    }
+  }
+  if (!q_ok) return;
+  if (a.splits == 1) {
+    const float inv = 1.0f / l_tot;
+    bf16 *orow = (bf16 *)a.O + (size_t)my_q * a.hidden + h * D;
+#pragma unroll
+    for (int t = 0; t < 3; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int d = t * 32 + i * 8 + g * 4;
+        if (d < D) {
+          bf16x4 v;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v[j] = (bf16)(o[t][i * 4 + j] * inv);
+          *(bf16x4 *)(orow + d) = v;
+        }
+      }
+  } else {
+    float *orow = a.Opart + ((size_t)split * a.total_rows + my_q) * a.hidden + h * D;
+#pragma unroll
+    for (int t = 0; t < 3; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int d = t * 32 + i * 8 + g * 4;
+        if (d < D) *(f32x4 *)(orow + d) = f32x4{o[t][i * 4], o[t][i * 4 + 1], o[t][i * 4 + 2], o[t][i * 4 + 3]};
+      }
+    if (g == 0) {
+      float *ml = a.ML + (((size_t)split * a.total_rows + my_q) * heads + h) * 2;
+      ml[0] = m_run * c2;  // log2-domain maximum, as the combine expects
+      ml[1] = l_tot;
+    }
+  }
+}
+
+hipError_t launch_attention2(const AttnArgs &a, int n_chains, int max_rows, bool cross, hipStream_t s) {
+  if (max_rows <= 0) return hipSuccess;
+  if (a.n_keys % A2_BK != 0 || a.splits < 1 || a.splits > a.n_keys / A2_BK) return hipErrorInvalidValue;
+  dim3 grid((max_rows + A2_BQ - 1) / A2_BQ, (a.hidden / kHeadDim) * a.splits, n_chains);
+  if (cross)
+    hipLaunchKernelGGL(attn2_kernel<true>, grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(attn2_kernel<false>, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace rc

@@ -1,0 +1,321 @@
+// bf16 matrix-core GEMM, second form: Y[M][N] = A[M][K] . W[N][K]^T over a
+// ragged row count M with the epilogues of the step (see rc_internal.h).
+//
+// * Operands move global -> LDS with global_load_lds_dwordx4 (no VGPR
+//   staging); every 128-byte K-row of a tile is stored with its eight
+//   16-byte chunks XOR-swizzled by (row & 7), so the MFMA fragment reads
+//   (lane l reads row l%32, chunk 2kk + l/32) hit distinct LDS banks.
+// * STAGES-deep ring of LDS buffers, one barrier per 64-wide K step; loads
+//   for step k+STAGES-1 are issued right after the barrier of step k.
+// * 256 threads = 4 waves in a 2x2 grid, each wave a (BM/2)x(BN/2) block of
+//   32x32x16 MFMAs.
+// * Split-K over grid.z: each split writes an fp32 partial tile and a
+//   separate kernel sums the splits in a fixed order and applies the
+//   epilogue, so results do not depend on scheduling.
+// * Tiles are renumbered so that consecutive logical tiles (all row tiles of
+//   one column panel of W) land on the same XCD (workgroups are dealt to the
+//   eight XCDs round-robin) and share that XCD's L2.
+#include "rc_common.h"
+#include "rc_internal.h"
+
+#include <cmath>
+
+namespace rc {
+
+constexpr int G2_BK = 64;  // bf16 elements per K step (128 bytes per row)
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Workgroup barrier without the memory fence of __syncthreads(): the fence
+// would make the compiler drain every in-flight global->LDS load before the
+// barrier.  Each thread waits for its own loads of the stage being consumed
+// (wait_vmcnt) before arriving; LDS reads of the previous stage have been
+// consumed by MFMAs, so they are complete.  The clobber keeps the compiler
+// from moving memory accesses across.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// Store one output element through the epilogue.
+template <int EPI>
+__device__ __forceinline__ void epi_store(const GemmArgs &g, int m, int n, float v, float gate, int part, int hh,
+                                          int dd) {
+  if (EPI == EPI_STORE) {
+    ((bf16 *)g.out)[(size_t)m * g.ldo + n] = (bf16)v;
+  } else if (EPI == EPI_GELU) {
+    ((bf16 *)g.out)[(size_t)m * g.ldo + n] = (bf16)gelu_tanh(v);
+  } else if (EPI == EPI_RESID) {
+    float *xp = g.X + (size_t)m * g.ldx + n;
+    const float x = *xp + gate * v;
+    *xp = x;
+    if (g.xt) ((bf16 *)g.xt)[(size_t)m * g.ldx + n] = (bf16)x;
+    if (g.hrows) ((bf16 *)g.hrows)[(size_t)m * g.N + n] = (bf16)x;
+    if (g.hslot) {
+      const int pk = g.rows[m];
+      ((bf16 *)g.hslot)[row_chain(pk) * g.chain_stride + (size_t)row_token(pk) * g.hidden + n] = (bf16)x;
+    }
+  } else if (EPI == EPI_QKV) {
+    if (part == 0) {
+      ((bf16 *)g.out)[(size_t)m * g.ldo + n] = (bf16)v;
+    } else {
+      const int pk = g.rows[m];
+      const size_t cb = (size_t)row_chain(pk) * g.chain_stride;
+      const int tok = row_token(pk);
+      if (part == 1)
+        ((bf16 *)g.kslot)[cb + ((size_t)hh * g.tokens + tok) * kHeadDim + dd] = (bf16)v;
+      else
+        ((bf16 *)g.vtslot)[cb + ((size_t)hh * kHeadDim + dd) * g.tokens + tok] = (bf16)v;
+    }
+  } else if (EPI == EPI_TEXTKV) {
+    const int b = m / g.text_len, t = m - b * g.text_len;
+    bf16 *base = (bf16 *)g.tkv + (size_t)b * g.tkv_chain_stride;
+    const size_t half = (size_t)(g.hidden / kHeadDim) * g.text_pad * kHeadDim;
+    if (part == 0)
+      base[((size_t)hh * g.text_pad + t) * kHeadDim + dd] = (bf16)v;
+    else
+      base[half + ((size_t)hh * kHeadDim + dd) * g.text_pad + t] = (bf16)v;
+  }
+}
+
+template <int EPI>
+__device__ __forceinline__ void col_info(const GemmArgs &g, int n, float &bn, float &gate, int &part, int &hh,
+                                         int &dd) {
+  bn = g.bias ? g.bias[n] : 0.0f;
+  gate = 1.0f;
+  if (EPI == EPI_RESID && g.gate) gate = g.gate[n] + (g.gate2 ? g.gate2[n] : 0.0f);
+  part = 0;
+  hh = 0;
+  dd = 0;
+  if (EPI == EPI_QKV || EPI == EPI_TEXTKV) {
+    part = n / g.hidden;
+    const int c = n - part * g.hidden;
+    hh = c / kHeadDim;
+    dd = c - hh * kHeadDim;
+  }
+}
+
+template <int BM, int BN, int STAGES, int EPI, bool SPLIT>
+__global__ __launch_bounds__(256, 2) void gemm2_kernel(GemmArgs g, float *partial, int k_per_split) {
+  constexpr int WM = BM / 2, WN = BN / 2, FM = WM / 32, FN = WN / 32;
+  constexpr int A_LD = BM * 8 / 256;  // direct loads per thread per stage (16 bytes each)
+  constexpr int B_LD = BN * 8 / 256;
+  constexpr int LPS = A_LD + B_LD;
+  constexpr int STAGE_BYTES = (BM + BN) * 128;
+  __shared__ __attribute__((aligned(1024))) char lds[STAGES * STAGE_BYTES];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  // XCD-aware tile order: logical tile L walks the row tiles of one column
+  // panel before moving to the next panel; physical id p runs on XCD p % 8.
+  const int tiles_m = gridDim.y, tiles_n = gridDim.x, T = tiles_m * tiles_n;
+  const int p = blockIdx.y * tiles_n + blockIdx.x;
+  int L = p;
+  if (T % 8 == 0) L = (p % 8) * (T / 8) + p / 8;
+  const int tn = L / tiles_m, tm = L - (L / tiles_m) * tiles_m;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int kbeg = blockIdx.z * k_per_split;
+  const int nk = k_per_split / G2_BK;
+
+  const bf16 *A = (const bf16 *)g.A;
+  const bf16 *W = (const bf16 *)g.W;
+
+  // per-thread load descriptors: chunk index -> (row, logical chunk)
+  auto issue = [&](int stage, int k0) {
+    char *sa = lds + stage * STAGE_BYTES;
+    char *sb = sa + BM * 128;
+#pragma unroll
+    for (int i = 0; i < A_LD; ++i) {
+      const int ch = (i * 4 + wave) * 64 + lane;
+      const int r = ch >> 3, c = (ch & 7) ^ (r & 7);
+      const int gr = min(m0 + r, g.M - 1);
+      const bf16 *src = A + (size_t)gr * g.lda + k0 + c * 8;
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
+                                       (__attribute__((address_space(3))) void *)(sa + (i * 4 + wave) * 1024), 16, 0,
+                                       0);
+    }
+#pragma unroll
+    for (int i = 0; i < B_LD; ++i) {
+      const int ch = (i * 4 + wave) * 64 + lane;
+      const int r = ch >> 3, c = (ch & 7) ^ (r & 7);
+      const bf16 *src = W + (size_t)(n0 + r) * g.K + k0 + c * 8;
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
+                                       (__attribute__((address_space(3))) void *)(sb + (i * 4 + wave) * 1024), 16, 0,
+                                       0);
+    }
+  };
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nk) issue(s, kbeg + s * G2_BK);
+
+  const int g32 = lane >> 5, r32 = lane & 31;
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + STAGES - 2 < nk) wait_vmcnt<(STAGES - 2) * LPS>();
+    else wait_vmcnt<0>();
+    lds_barrier();
+    if (kt + STAGES - 1 < nk) issue((kt + STAGES - 1) % STAGES, kbeg + (kt + STAGES - 1) * G2_BK);
+    const char *sa = lds + (kt % STAGES) * STAGE_BYTES;
+    const char *sb = sa + BM * 128;
+    // fragments of sub-step kk+1 are read while the MFMAs of kk run
+    bf16x8 a[2][FM], b[2][FN];
+    auto frags = [&](int buf, int kk) {
+      const int c = kk * 2 + g32;
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const int r = wm * WM + i * 32 + r32;
+        a[buf][i] = *(const bf16x8 *)(sa + r * 128 + ((c ^ (r & 7)) << 4));
+      }
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int r = wn * WN + j * 32 + r32;
+        b[buf][j] = *(const bf16x8 *)(sb + r * 128 + ((c ^ (r & 7)) << 4));
+      }
+    };
+    frags(0, 0);
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      if (kk < 3) frags((kk + 1) & 1, kk + 1);
+      // keep the reads of kk+1 ahead of the MFMAs of kk (the scheduler would
+      // otherwise sink them and reuse one register set)
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk & 1][i], b[kk & 1][j], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+
+  if (SPLIT) {
+    float *P = partial + (size_t)blockIdx.z * g.M * g.N;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int n = n0 + wn * WN + j * 32 + r32;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int m = m0 + wm * WM + i * 32 + (e >> 2) * 8 + g32 * 4 + (e & 3);
+          if (m < g.M) P[(size_t)m * g.N + n] = acc[i][j][e];
+        }
+    }
+    return;
+  }
+#pragma unroll
+  for (int j = 0; j < FN; ++j) {
+    const int n = n0 + wn * WN + j * 32 + r32;
+    float bn, gate;
+    int part, hh, dd;
+    col_info<EPI>(g, n, bn, gate, part, hh, dd);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int m = m0 + wm * WM + i * 32 + (e >> 2) * 8 + g32 * 4 + (e & 3);
+        if (m < g.M) epi_store<EPI>(g, m, n, acc[i][j][e] + bn, gate, part, hh, dd);
+      }
+  }
+}
+
+// Sum of the split partials in split order, then the epilogue.  One thread
+// per output element; consecutive threads walk n.
+template <int EPI>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs g, const float *partial, int splits) {
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (long)g.M * g.N) return;
+  const int m = idx / g.N, n = idx - (long)m * g.N;
+  float v = 0.0f;
+  for (int s = 0; s < splits; ++s) v += partial[(size_t)s * g.M * g.N + idx];
+  float bn, gate;
+  int part, hh, dd;
+  col_info<EPI>(g, n, bn, gate, part, hh, dd);
+  epi_store<EPI>(g, m, n, v + bn, gate, part, hh, dd);
+}
+
+template <int BM, int BN, int STAGES, bool SPLIT>
+static void launch_g2(const GemmArgs &a, int epi, int splits, float *partial, hipStream_t s) {
+  dim3 grid(a.N / BN, (a.M + BM - 1) / BM, splits);
+  const int kps = a.K / splits;
+#define RC_G2(E) hipLaunchKernelGGL((gemm2_kernel<BM, BN, STAGES, E, SPLIT>), grid, dim3(256), 0, s, a, partial, kps)
+  switch (epi) {
+    case EPI_STORE: RC_G2(EPI_STORE); break;
+    case EPI_GELU: RC_G2(EPI_GELU); break;
+    case EPI_RESID: RC_G2(EPI_RESID); break;
+    case EPI_QKV: RC_G2(EPI_QKV); break;
+    case EPI_TEXTKV: RC_G2(EPI_TEXTKV); break;
+  }
+#undef RC_G2
+}
+
+static void launch_reduce(const GemmArgs &a, int epi, int splits, const float *partial, hipStream_t s) {
+  const long n = (long)a.M * a.N;
+  dim3 grid((n + 255) / 256);
+#define RC_RD(E) hipLaunchKernelGGL(splitk_reduce_kernel<E>, grid, dim3(256), 0, s, a, partial, splits)
+  switch (epi) {
+    case EPI_STORE: RC_RD(EPI_STORE); break;
+    case EPI_GELU: RC_RD(EPI_GELU); break;
+    case EPI_RESID: RC_RD(EPI_RESID); break;
+    case EPI_QKV: RC_RD(EPI_QKV); break;
+    case EPI_TEXTKV: RC_RD(EPI_TEXTKV); break;
+  }
+#undef RC_RD
+}
+
+// Choice of tile and split count for a shape: the candidate with the best
+// occupancy of 2 workgroups x 256 CUs per wave of the grid, preferring fewer
+// splits, with every split at least 4 K steps long.
+GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats) {
+  GemmPlan best{128, 128, 1};
+  double best_score = -1.0;
+  const int nk = K / G2_BK;
+  const int bms[2] = {128, 64};
+  for (int bm : bms) {
+    if (N % 128) continue;
+    const long tiles = (long)((M + bm - 1) / bm) * (N / 128);
+    for (int s = 1; s <= 16; ++s) {
+      if (nk % s || nk / s < 4) continue;
+      if (s > 1 && (size_t)s * M * N > partial_cap_floats) continue;
+      const long wgs = tiles * s;
+      const double slots = 512.0;
+      const double waves = std::ceil(wgs / slots);
+      double eff = wgs / (waves * slots);
+      // per-workgroup efficiency falls for small tiles and short K ranges
+      eff *= (bm == 128 ? 1.0 : 0.8) * (1.0 - 0.04 * (s - 1)) * std::min(1.0, (nk / s) / 6.0 + 0.5);
+      if (eff > best_score + 1e-9) {
+        best_score = eff;
+        best = GemmPlan{bm, 128, s};
+      }
+    }
+  }
+  return best;
+}
+
+hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &pl, float *partial, hipStream_t s) {
+  if (a.M <= 0) return hipSuccess;
+  if (a.N % pl.bn || a.K % (G2_BK * pl.splits)) return hipErrorInvalidValue;
+  const bool split = pl.splits > 1;
+  if (pl.bm == 128) {
+    if (split) launch_g2<128, 128, 2, true>(a, epi, pl.splits, partial, s);
+    else launch_g2<128, 128, 2, false>(a, epi, 1, nullptr, s);
+  } else {
+    if (split) launch_g2<64, 128, 3, true>(a, epi, pl.splits, partial, s);
+    else launch_g2<64, 128, 3, false>(a, epi, 1, nullptr, s);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !split) return e;
+  launch_reduce(a, epi, pl.splits, partial, s);
+  return hipGetLastError();
+}
+
+}  // namespace rc

@@ -66,8 +66,17 @@ struct AttnArgs {
 };
 
 template <typename T> hipError_t launch_gemm(const GemmArgs &a, int epi, hipStream_t s);
+
+// bf16 GEMM with direct-to-LDS staging and optional split-K (rc_gemm2.hip).
+struct GemmPlan {
+  int bm, bn, splits;
+};
+GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats);
+hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &plan, float *partial, hipStream_t s);
 template <typename T> hipError_t launch_attention(const AttnArgs &a, int n_chains, int max_rows,
                                                   bool emit_maps, hipStream_t s);
+// bf16 attention with direct-to-LDS tiles and uneven key splits (rc_attn2.hip).
+hipError_t launch_attention2(const AttnArgs &a, int n_chains, int max_rows, bool cross, hipStream_t s);
 hipError_t launch_attn_combine(const float *Opart, const float *ML, void *O, bool bf16_out, int R,
                                int heads, int splits, hipStream_t s);
 hipError_t launch_maps_reduce(const float *pmaps, const int *rows, float *maps, int R, int heads,
