@@ -255,24 +255,43 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   }
 }
 
-// Deterministic combine of key-split partials: O = sum_s 2^(m_s-M) o_s / sum_s 2^(m_s-M) l_s.
+// Deterministic combine of key-split partials: O = sum_s 2^(m_s-M) o_s / sum_s
+// 2^(m_s-M) l_s, in split order.  One thread per (row, head, 4 dims).
+template <typename T> __device__ __forceinline__ void put4(T *p, const float *v);
+template <> __device__ __forceinline__ void put4<float>(float *p, const float *v) {
+  *(f32x4 *)p = f32x4{v[0], v[1], v[2], v[3]};
+}
+template <> __device__ __forceinline__ void put4<bf16>(bf16 *p, const float *v) {
+  bf16x4 o;
+  o[0] = (bf16)v[0]; o[1] = (bf16)v[1]; o[2] = (bf16)v[2]; o[3] = (bf16)v[3];
+  *(bf16x4 *)p = o;
+}
+
 template <typename T>
-__global__ void attn_combine_kernel(const float *Opart, const float *ML, T *O, int R, int heads,
-                                    int splits) {
+__global__ void attn_combine_kernel(const float *Opart, const float *ML, T *O, int R, int heads, int splits) {
+  constexpr int G = kHeadDim / 4;
   const int C = heads * kHeadDim;
   const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (long)R * C) return;
-  const int r = idx / C, c = idx - (long)r * C, h = c / kHeadDim;
+  if (idx >= (long)R * heads * G) return;
+  const int r = idx / (heads * G);
+  const int rem = idx - (long)r * heads * G;
+  const int h = rem / G, d = (rem - h * G) * 4;
   float M = -INFINITY;
   for (int s = 0; s < splits; ++s) M = fmaxf(M, ML[(((size_t)s * R + r) * heads + h) * 2]);
-  float num = 0.0f, den = 0.0f;
+  float num[4] = {0.0f, 0.0f, 0.0f, 0.0f}, den = 0.0f;
   for (int s = 0; s < splits; ++s) {
     const float *ml = ML + (((size_t)s * R + r) * heads + h) * 2;
     const float w = exp2f(ml[0] - M);
-    num += w * Opart[((size_t)s * R + r) * C + c];
+    const f32x4 p = *(const f32x4 *)(Opart + ((size_t)s * R + r) * C + h * kHeadDim + d);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) num[k] += w * p[k];
     den += w * ml[1];
   }
-  O[(size_t)r * C + c] = from_f<T>(num / den);
+  const float inv = 1.0f / den;
+  float v[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) v[k] = num[k] * inv;
+  put4<T>(O + (size_t)r * C + h * kHeadDim + d, v);
 }
 
 // maps[chain][token][j] += sum over heads (fixed order) of the per-head
@@ -306,7 +325,7 @@ template hipError_t launch_attention<float>(const AttnArgs &, int, int, bool, hi
 hipError_t launch_attn_combine(const float *Opart, const float *ML, void *O, bool bf16_out, int R,
                                int heads, int splits, hipStream_t s) {
   if (R <= 0) return hipSuccess;
-  const long n = (long)R * heads * kHeadDim;
+  const long n = (long)R * heads * (kHeadDim / 4);
   dim3 grid((n + 255) / 256);
   if (bf16_out)
     hipLaunchKernelGGL(attn_combine_kernel<bf16>, grid, dim3(256), 0, s, Opart, ML, (bf16 *)O, R, heads, splits);

@@ -82,39 +82,61 @@ template hipError_t launch_embed<bf16>(const EmbedArgs &, int, hipStream_t);
 template hipError_t launch_embed<float>(const EmbedArgs &, int, hipStream_t);
 
 // out[r][:] = E( LN(X[r]) * (1 + scale) + shift ), scale/shift = table row + t0
-// row.  One wave per row; statistics in fp32 with a two-pass variance.
+// row.  One wave per row, 16-byte accesses; statistics in fp32 with a
+// two-pass variance over the values held in registers.
+template <typename T> __device__ __forceinline__ void store4(T *p, float a, float b, float c, float d);
+template <> __device__ __forceinline__ void store4<float>(float *p, float a, float b, float c, float d) {
+  *(f32x4 *)p = f32x4{a, b, c, d};
+}
+template <> __device__ __forceinline__ void store4<bf16>(bf16 *p, float a, float b, float c, float d) {
+  bf16x4 v;
+  v[0] = (bf16)a; v[1] = (bf16)b; v[2] = (bf16)c; v[3] = (bf16)d;
+  *(bf16x4 *)p = v;
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void ln_mod_kernel(const float *X, int R, int C, const float *table,
                                                      const float *t0, int shift_row, float eps, T *out) {
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (r >= R) return;
-  const float *x = X + (size_t)r * C;
-  constexpr int MAXV = 24;  // C <= 64*MAXV
-  float v[MAXV];
+  constexpr int MAXV = 6;  // C <= 64*4*MAXV
+  const int C4 = C >> 2;
+  const f32x4 *x = (const f32x4 *)(X + (size_t)r * C);
+  f32x4 v[MAXV];
   float s = 0.0f;
 #pragma unroll
   for (int i = 0; i < MAXV; ++i) {
     const int n = lane + i * 64;
-    v[i] = n < C ? x[n] : 0.0f;
-    s += v[i];
+    v[i] = n < C4 ? x[n] : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
   }
   const float mean = wave_sum(s) / C;
   float q = 0.0f;
 #pragma unroll
   for (int i = 0; i < MAXV; ++i) {
     const int n = lane + i * 64;
-    const float d = n < C ? v[i] - mean : 0.0f;
-    q += d * d;
+    if (n < C4)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float d = v[i][k] - mean;
+        q += d * d;
+      }
   }
   const float rstd = rsqrtf(wave_sum(q) / C + eps);
-  const float *sh = table + (size_t)shift_row * C, *sc = sh + C;
-  const float *tsh = t0 + (size_t)shift_row * C, *tsc = tsh + C;
+  const f32x4 *sh = (const f32x4 *)(table + (size_t)shift_row * C), *sc = (const f32x4 *)(table + (size_t)(shift_row + 1) * C);
+  const f32x4 *tsh = (const f32x4 *)(t0 + (size_t)shift_row * C), *tsc = (const f32x4 *)(t0 + (size_t)(shift_row + 1) * C);
   T *o = out + (size_t)r * C;
 #pragma unroll
   for (int i = 0; i < MAXV; ++i) {
     const int n = lane + i * 64;
-    if (n < C) o[n] = from_f<T>((v[i] - mean) * rstd * (1.0f + sc[n] + tsc[n]) + sh[n] + tsh[n]);
+    if (n < C4) {
+      const f32x4 a = sh[n], b = sc[n], ta = tsh[n], tb = tsc[n];
+      float y[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) y[k] = (v[i][k] - mean) * rstd * (1.0f + b[k] + tb[k]) + a[k] + ta[k];
+      store4<T>(o + 4 * n, y[0], y[1], y[2], y[3]);
+    }
   }
 }
 
@@ -122,7 +144,7 @@ template <typename T>
 hipError_t launch_ln_mod(const float *X, int R, int C, const float *table, const float *t0, int shift_row,
                          float eps, void *out, hipStream_t s) {
   if (R <= 0) return hipSuccess;
-  if (C > 64 * 24) return hipErrorInvalidValue;
+  if (C > 64 * 4 * 6 || C % 4) return hipErrorInvalidValue;
   hipLaunchKernelGGL(ln_mod_kernel<T>, dim3((R + 3) / 4), dim3(256), 0, s, X, R, C, table, t0, shift_row, eps,
                      (T *)out);
   return hipGetLastError();

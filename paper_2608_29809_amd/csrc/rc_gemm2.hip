@@ -78,6 +78,64 @@ __device__ __forceinline__ void epi_store(const GemmArgs &g, int m, int n, float
   }
 }
 
+__device__ __forceinline__ void st4(bf16 *p, const float *v) {
+  bf16x4 o;
+  o[0] = (bf16)v[0]; o[1] = (bf16)v[1]; o[2] = (bf16)v[2]; o[3] = (bf16)v[3];
+  *(bf16x4 *)p = o;
+}
+
+// Four consecutive output columns n..n+3 of row m (n % 4 == 0; never the
+// transposed-V part, whose columns are handled one by one).
+template <int EPI>
+__device__ __forceinline__ void epi4(const GemmArgs &g, int m, int n, float *v, int part) {
+  if (EPI == EPI_STORE) {
+    st4((bf16 *)g.out + (size_t)m * g.ldo + n, v);
+  } else if (EPI == EPI_GELU) {
+    float w[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) w[q] = gelu_tanh(v[q]);
+    st4((bf16 *)g.out + (size_t)m * g.ldo + n, w);
+  } else if (EPI == EPI_RESID) {
+    f32x4 gt = f32x4{1.0f, 1.0f, 1.0f, 1.0f};
+    if (g.gate) {
+      gt = *(const f32x4 *)(g.gate + n);
+      if (g.gate2) {
+        const f32x4 g2 = *(const f32x4 *)(g.gate2 + n);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) gt[q] += g2[q];
+      }
+    }
+    f32x4 *xp = (f32x4 *)(g.X + (size_t)m * g.ldx + n);
+    f32x4 x = *xp;
+    float xs[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      x[q] += gt[q] * v[q];
+      xs[q] = x[q];
+    }
+    *xp = x;
+    if (g.xt) st4((bf16 *)g.xt + (size_t)m * g.ldx + n, xs);
+    if (g.hrows) st4((bf16 *)g.hrows + (size_t)m * g.N + n, xs);
+    if (g.hslot) {
+      const int pk = g.rows[m];
+      st4((bf16 *)g.hslot + row_chain(pk) * g.chain_stride + (size_t)row_token(pk) * g.hidden + n, xs);
+    }
+  } else if (EPI == EPI_QKV) {
+    if (part == 0) {
+      st4((bf16 *)g.out + (size_t)m * g.ldo + n, v);
+    } else {
+      const int pk = g.rows[m];
+      const int c = n - g.hidden, hh = c / kHeadDim, dd = c - hh * kHeadDim;
+      st4((bf16 *)g.kslot + (size_t)row_chain(pk) * g.chain_stride +
+              ((size_t)hh * g.tokens + row_token(pk)) * kHeadDim + dd, v);
+    }
+  } else if (EPI == EPI_TEXTKV) {
+    const int b = m / g.text_len, t = m - b * g.text_len;
+    const int hh = n / kHeadDim, dd = n - hh * kHeadDim;
+    st4((bf16 *)g.tkv + (size_t)b * g.tkv_chain_stride + ((size_t)hh * g.text_pad + t) * kHeadDim + dd, v);
+  }
+}
+
 template <int EPI>
 __device__ __forceinline__ void col_info(const GemmArgs &g, int n, float &bn, float &gate, int &part, int &hh,
                                          int &dd) {
@@ -212,19 +270,50 @@ __global__ __launch_bounds__(256, 2) void gemm2_kernel(GemmArgs g, float *partia
     }
     return;
   }
+  // Output tile through LDS (the stage buffers are free: every load has been
+  // consumed), then written back with 16-byte row-contiguous accesses; tiles
+  // of a transposed-V output are walked column-major instead so consecutive
+  // threads write consecutive tokens.
+  constexpr int CLD = BN + 4;
+  static_assert(BM * CLD * 4 <= STAGES * STAGE_BYTES, "output tile must fit the stage buffers");
+  __syncthreads();
+  float *ct = (float *)lds;
 #pragma unroll
-  for (int j = 0; j < FN; ++j) {
-    const int n = n0 + wn * WN + j * 32 + r32;
-    float bn, gate;
-    int part, hh, dd;
-    col_info<EPI>(g, n, bn, gate, part, hh, dd);
+  for (int j = 0; j < FN; ++j)
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int m = m0 + wm * WM + i * 32 + (e >> 2) * 8 + g32 * 4 + (e & 3);
-        if (m < g.M) epi_store<EPI>(g, m, n, acc[i][j][e] + bn, gate, part, hh, dd);
+      for (int e = 0; e < 16; ++e)
+        ct[(wm * WM + i * 32 + (e >> 2) * 8 + g32 * 4 + (e & 3)) * CLD + wn * WN + j * 32 + r32] = acc[i][j][e];
+  __syncthreads();
+  const int tile_part = (EPI == EPI_QKV || EPI == EPI_TEXTKV) ? n0 / g.hidden : 0;
+  const bool transposed = (EPI == EPI_QKV && tile_part == 2) || (EPI == EPI_TEXTKV && tile_part == 1);
+  if (!transposed) {
+#pragma unroll
+    for (int k = 0; k < BM * BN / 4 / 256; ++k) {
+      const int idx = tid + k * 256, row = idx / (BN / 4), c4 = (idx % (BN / 4)) * 4;
+      const int m = m0 + row;
+      if (m >= g.M) continue;
+      const int n = n0 + c4;
+      const f32x4 bb = g.bias ? *(const f32x4 *)(g.bias + n) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+      float v[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] = ct[row * CLD + c4 + q] + bb[q];
+      epi4<EPI>(g, m, n, v, tile_part);
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < BM * BN / 4 / 256; ++k) {
+      const int idx = tid + k * 256, col = idx / (BM / 4), r4 = (idx % (BM / 4)) * 4;
+      const int n = n0 + col;
+      const float bn = g.bias ? g.bias[n] : 0.0f;
+      const int c = n - tile_part * g.hidden, hh = c / kHeadDim, dd = c - hh * kHeadDim;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int m = m0 + r4 + q;
+        if (m < g.M) epi_store<EPI>(g, m, n, ct[(r4 + q) * CLD + col] + bn, 1.0f, tile_part, hh, dd);
       }
+    }
   }
 }
 
@@ -272,46 +361,25 @@ static void launch_reduce(const GemmArgs &a, int epi, int splits, const float *p
 #undef RC_RD
 }
 
-// Choice of tile and split count for a shape: the candidate with the best
-// occupancy of 2 workgroups x 256 CUs per wave of the grid, preferring fewer
-// splits, with every split at least 4 K steps long.
+// Choice of tile and split count for a shape.  Measured on the step's shapes
+// (723 and 4096 rows, N in {1152, 3456, 4608}, K in {1152, 4608}): 64x128
+// tiles beat 128x128 everywhere but one shape (within 4 %), and split-K only
+// pays for K = 4608 when the grid is short of workgroups (the partial sums and
+// their reduction cost more than the idle CUs otherwise).
 GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats) {
-  GemmPlan best{128, 128, 1};
-  double best_score = -1.0;
+  GemmPlan p{64, 128, 1};
+  const long tiles = (long)((M + 63) / 64) * (N / 128);
   const int nk = K / G2_BK;
-  const int bms[2] = {128, 64};
-  for (int bm : bms) {
-    if (N % 128) continue;
-    const long tiles = (long)((M + bm - 1) / bm) * (N / 128);
-    for (int s = 1; s <= 16; ++s) {
-      if (nk % s || nk / s < 4) continue;
-      if (s > 1 && (size_t)s * M * N > partial_cap_floats) continue;
-      const long wgs = tiles * s;
-      const double slots = 512.0;
-      const double waves = std::ceil(wgs / slots);
-      double eff = wgs / (waves * slots);
-      // per-workgroup efficiency falls for small tiles and short K ranges
-      eff *= (bm == 128 ? 1.0 : 0.8) * (1.0 - 0.04 * (s - 1)) * std::min(1.0, (nk / s) / 6.0 + 0.5);
-      if (eff > best_score + 1e-9) {
-        best_score = eff;
-        best = GemmPlan{bm, 128, s};
-      }
-    }
-  }
-  return best;
+  if (K >= 2048 && tiles < 384 && nk % 2 == 0 && (size_t)2 * M * N <= partial_cap_floats) p.splits = 2;
+  return p;
 }
 
 hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &pl, float *partial, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
-  if (a.N % pl.bn || a.K % (G2_BK * pl.splits)) return hipErrorInvalidValue;
+  if (pl.bm != 64 || pl.bn != 128 || a.N % 128 || a.K % (G2_BK * pl.splits)) return hipErrorInvalidValue;
   const bool split = pl.splits > 1;
-  if (pl.bm == 128) {
-    if (split) launch_g2<128, 128, 2, true>(a, epi, pl.splits, partial, s);
-    else launch_g2<128, 128, 2, false>(a, epi, 1, nullptr, s);
-  } else {
-    if (split) launch_g2<64, 128, 3, true>(a, epi, pl.splits, partial, s);
-    else launch_g2<64, 128, 3, false>(a, epi, 1, nullptr, s);
-  }
+  if (split) launch_g2<64, 128, 3, true>(a, epi, pl.splits, partial, s);
+  else launch_g2<64, 128, 2, false>(a, epi, 1, nullptr, s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !split) return e;
   launch_reduce(a, epi, pl.splits, partial, s);
