@@ -200,71 +200,84 @@ template hipError_t launch_gemv<float>(const void *, const float *, const float 
 
 // Final layer + DDIM for each computed row: eps = (LN(X)(1+sc)+sh) W_f^T + b_f
 // for the noise channels of the 2x2 patch, then x' = ca * x + cb * eps written
-// to the output latent and (if given) to the cached trajectory entry.
+// to the output latent and (if given) to the cached trajectory entry.  A
+// workgroup stages the 16 noise rows of W_f in LDS once and serves 8 rows
+// (two per wave); each output is a wave-wide dot product.
+constexpr int FIN_ROWS = 8;
+
 template <typename T>
 __global__ __launch_bounds__(256) void final_ddim_kernel(FinalArgs a) {
-  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (r >= a.R) return;
-  const int C = a.C;
-  const float *x = a.X + (size_t)r * C;
-  constexpr int MAXV = 24;
-  float v[MAXV];
-  float s = 0.0f;
-#pragma unroll
-  for (int i = 0; i < MAXV; ++i) {
-    const int n = lane + i * 64;
-    v[i] = n < C ? x[n] : 0.0f;
-    s += v[i];
-  }
-  const float mean = wave_sum(s) / C;
-  float q = 0.0f;
-#pragma unroll
-  for (int i = 0; i < MAXV; ++i) {
-    const int n = lane + i * 64;
-    const float d = n < C ? v[i] - mean : 0.0f;
-    q += d * d;
-  }
-  const float rstd = rsqrtf(wave_sum(q) / C + a.eps);
-#pragma unroll
-  for (int i = 0; i < MAXV; ++i) {
-    const int n = lane + i * 64;
-    if (n < C) {
-      const float sh = a.fin_sst[n] + a.t_emb[n];
-      const float sc = a.fin_sst[C + n] + a.t_emb[n];
-      v[i] = (v[i] - mean) * rstd * (1.0f + sc) + sh;
-    }
-  }
-  const int pk = a.rows[r];
-  const int b = row_chain(pk), tok = row_token(pk);
-  const int y = tok / a.gw, xx = tok - y * a.gw;
-  const int Hl = a.gh * 2, Wl = a.gw * 2;
+  extern __shared__ __attribute__((aligned(16))) char fin_lds[];
+  T *wl = (T *)fin_lds;  // [16][C]: output o = pix*4 + c is W_f row pix*out_ch + c
+  const int C = a.C, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const T *W = (const T *)a.fin_w;
-  for (int pix = 0; pix < 4; ++pix) {
-    const int pi = pix >> 1, qi = pix & 1;
-    for (int c = 0; c < 4; ++c) {
-      const int o = pix * a.out_ch + c;
+  for (int i = threadIdx.x; i < 16 * C; i += 256) {
+    const int o = i / C, n = i - o * C;
+    wl[i] = W[(size_t)((o >> 2) * a.out_ch + (o & 3)) * C + n];
+  }
+  __syncthreads();
+  constexpr int MAXV = 24;
+  for (int rr = 0; rr < FIN_ROWS / 4; ++rr) {
+    const int r = blockIdx.x * FIN_ROWS + wave * (FIN_ROWS / 4) + rr;
+    if (r >= a.R) break;
+    const float *x = a.X + (size_t)r * C;
+    float v[MAXV];
+    float s = 0.0f;
+#pragma unroll
+    for (int i = 0; i < MAXV; ++i) {
+      const int n = lane + i * 64;
+      v[i] = n < C ? x[n] : 0.0f;
+      s += v[i];
+    }
+    const float mean = wave_sum(s) / C;
+    float q = 0.0f;
+#pragma unroll
+    for (int i = 0; i < MAXV; ++i) {
+      const int n = lane + i * 64;
+      const float d = n < C ? v[i] - mean : 0.0f;
+      q += d * d;
+    }
+    const float rstd = rsqrtf(wave_sum(q) / C + a.eps);
+#pragma unroll
+    for (int i = 0; i < MAXV; ++i) {
+      const int n = lane + i * 64;
+      if (n < C) v[i] = (v[i] - mean) * rstd * (1.0f + a.fin_sst[C + n] + a.t_emb[n]) + a.fin_sst[n] + a.t_emb[n];
+    }
+    float eps[16];
+#pragma unroll
+    for (int o = 0; o < 16; ++o) {
       float acc = 0.0f;
 #pragma unroll
       for (int i = 0; i < MAXV; ++i) {
         const int n = lane + i * 64;
-        if (n < C) acc += v[i] * to_f<T>(W[(size_t)o * C + n]);
+        if (n < C) acc += v[i] * to_f<T>(wl[o * C + n]);
       }
-      acc = wave_sum(acc) + a.fin_b[o];
-      if (lane == 0) {
-        const size_t li = (((size_t)b * 4 + c) * Hl + 2 * y + pi) * Wl + 2 * xx + qi;
-        const float xn = a.ca * a.latent_in[li] + a.cb * acc;
-        a.latent_out[li] = xn;
-        if (a.traj_next) a.traj_next[b * a.traj_chain_stride + (li - (size_t)b * 4 * Hl * Wl)] = xn;
-      }
+      eps[o] = wave_sum(acc);
+    }
+    if (lane < 16) {
+      const int o = lane, pix = o >> 2, c = o & 3, pi = pix >> 1, qi = pix & 1;
+      float e = 0.0f;
+#pragma unroll
+      for (int k = 0; k < 16; ++k)
+        if (k == o) e = eps[k];
+      e += a.fin_b[pix * a.out_ch + c];
+      const int pk = a.rows[r];
+      const int b = row_chain(pk), tok = row_token(pk);
+      const int y = tok / a.gw, xx = tok - y * a.gw;
+      const int Hl = a.gh * 2, Wl = a.gw * 2;
+      const size_t li = (((size_t)b * 4 + c) * Hl + 2 * y + pi) * Wl + 2 * xx + qi;
+      const float xn = a.ca * a.latent_in[li] + a.cb * e;
+      a.latent_out[li] = xn;
+      if (a.traj_next) a.traj_next[b * a.traj_chain_stride + (li - (size_t)b * 4 * Hl * Wl)] = xn;
     }
   }
 }
 
 template <typename T> hipError_t launch_final_ddim(const FinalArgs &a, hipStream_t s) {
   if (a.R <= 0) return hipSuccess;
-  if (a.C > 64 * 24) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(final_ddim_kernel<T>, dim3((a.R + 3) / 4), dim3(256), 0, s, a);
+  if (a.C > 64 * 24 || a.out_ch < 4) return hipErrorInvalidValue;
+  const size_t lds = (size_t)16 * a.C * sizeof(T);
+  hipLaunchKernelGGL(final_ddim_kernel<T>, dim3((a.R + FIN_ROWS - 1) / FIN_ROWS), dim3(256), lds, s, a);
   return hipGetLastError();
 }
 template hipError_t launch_final_ddim<bf16>(const FinalArgs &, hipStream_t);

@@ -153,17 +153,21 @@ __device__ __forceinline__ void col_info(const GemmArgs &g, int n, float &bn, fl
   }
 }
 
-template <int BM, int BN, int STAGES, int EPI, bool SPLIT>
-__global__ __launch_bounds__(256, 2) void gemm2_kernel(GemmArgs g, float *partial, int k_per_split) {
+template <int BM, int BN, int STAGES, int KG, int EPI, bool SPLIT>
+__global__ __launch_bounds__(256 * KG) void gemm2_kernel(GemmArgs g, float *partial, int k_per_split) {
   constexpr int WM = BM / 2, WN = BN / 2, FM = WM / 32, FN = WN / 32;
   constexpr int A_LD = BM * 8 / 256;  // direct loads per thread per stage (16 bytes each)
   constexpr int B_LD = BN * 8 / 256;
   constexpr int LPS = A_LD + B_LD;
   constexpr int STAGE_BYTES = (BM + BN) * 128;
-  __shared__ __attribute__((aligned(1024))) char lds[STAGES * STAGE_BYTES];
+  constexpr int GROUP_BYTES = STAGES * STAGE_BYTES;  // one K group's ring
+  constexpr int CLD = BN + 4;                         // row of an fp32 output tile in LDS
+  static_assert(BM * CLD * 4 <= GROUP_BYTES, "output tile must fit a group's ring");
+  __shared__ __attribute__((aligned(1024))) char lds[KG * GROUP_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int kgrp = wave >> 2, w4 = wave & 3, t4 = tid & 255;
+  const int wm = w4 >> 1, wn = w4 & 1;
 
   // XCD-aware tile order: logical tile L walks the row tiles of one column
   // panel before moving to the next panel; physical id p runs on XCD p % 8.
@@ -173,34 +177,34 @@ __global__ __launch_bounds__(256, 2) void gemm2_kernel(GemmArgs g, float *partia
   if (T % 8 == 0) L = (p % 8) * (T / 8) + p / 8;
   const int tn = L / tiles_m, tm = L - (L / tiles_m) * tiles_m;
   const int m0 = tm * BM, n0 = tn * BN;
-  const int kbeg = blockIdx.z * k_per_split;
-  const int nk = k_per_split / G2_BK;
+  // K group kgrp covers its own contiguous share of this split's K range
+  const int kps_g = k_per_split / KG;
+  const int kbeg = blockIdx.z * k_per_split + kgrp * kps_g;
+  const int nk = kps_g / G2_BK;
+  char *ring = lds + kgrp * GROUP_BYTES;
 
   const bf16 *A = (const bf16 *)g.A;
   const bf16 *W = (const bf16 *)g.W;
 
-  // per-thread load descriptors: chunk index -> (row, logical chunk)
   auto issue = [&](int stage, int k0) {
-    char *sa = lds + stage * STAGE_BYTES;
+    char *sa = ring + stage * STAGE_BYTES;
     char *sb = sa + BM * 128;
 #pragma unroll
     for (int i = 0; i < A_LD; ++i) {
-      const int ch = (i * 4 + wave) * 64 + lane;
+      const int ch = (i * 4 + w4) * 64 + lane;
       const int r = ch >> 3, c = (ch & 7) ^ (r & 7);
       const int gr = min(m0 + r, g.M - 1);
       const bf16 *src = A + (size_t)gr * g.lda + k0 + c * 8;
       __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
-                                       (__attribute__((address_space(3))) void *)(sa + (i * 4 + wave) * 1024), 16, 0,
-                                       0);
+                                       (__attribute__((address_space(3))) void *)(sa + (i * 4 + w4) * 1024), 16, 0, 0);
     }
 #pragma unroll
     for (int i = 0; i < B_LD; ++i) {
-      const int ch = (i * 4 + wave) * 64 + lane;
+      const int ch = (i * 4 + w4) * 64 + lane;
       const int r = ch >> 3, c = (ch & 7) ^ (r & 7);
       const bf16 *src = W + (size_t)(n0 + r) * g.K + k0 + c * 8;
       __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
-                                       (__attribute__((address_space(3))) void *)(sb + (i * 4 + wave) * 1024), 16, 0,
-                                       0);
+                                       (__attribute__((address_space(3))) void *)(sb + (i * 4 + w4) * 1024), 16, 0, 0);
     }
   };
 
@@ -222,7 +226,7 @@ __global__ __launch_bounds__(256, 2) void gemm2_kernel(GemmArgs g, float *partia
     else wait_vmcnt<0>();
     lds_barrier();
     if (kt + STAGES - 1 < nk) issue((kt + STAGES - 1) % STAGES, kbeg + (kt + STAGES - 1) * G2_BK);
-    const char *sa = lds + (kt % STAGES) * STAGE_BYTES;
+    const char *sa = ring + (kt % STAGES) * STAGE_BYTES;
     const char *sb = sa + BM * 128;
     // fragments of sub-step kk+1 are read while the MFMAs of kk run
     bf16x8 a[2][FM], b[2][FN];
@@ -255,29 +259,13 @@ __global__ __launch_bounds__(256, 2) void gemm2_kernel(GemmArgs g, float *partia
     }
   }
 
-  if (SPLIT) {
-    float *P = partial + (size_t)blockIdx.z * g.M * g.N;
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const int n = n0 + wn * WN + j * 32 + r32;
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int m = m0 + wm * WM + i * 32 + (e >> 2) * 8 + g32 * 4 + (e & 3);
-          if (m < g.M) P[(size_t)m * g.N + n] = acc[i][j][e];
-        }
-    }
-    return;
-  }
-  // Output tile through LDS (the stage buffers are free: every load has been
-  // consumed), then written back with 16-byte row-contiguous accesses; tiles
-  // of a transposed-V output are walked column-major instead so consecutive
+  // Each K group's tile goes to LDS (the rings are free: every load has been
+  // consumed); the groups' tiles are summed in group order while the tile is
+  // written back with 16-byte row-contiguous accesses.  Tiles of a
+  // transposed-V output are walked column-major instead so that consecutive
   // threads write consecutive tokens.
-  constexpr int CLD = BN + 4;
-  static_assert(BM * CLD * 4 <= STAGES * STAGE_BYTES, "output tile must fit the stage buffers");
   __syncthreads();
-  float *ct = (float *)lds;
+  float *ct = (float *)ring;
 #pragma unroll
   for (int j = 0; j < FN; ++j)
 #pragma unroll
@@ -286,35 +274,54 @@ __global__ __launch_bounds__(256, 2) void gemm2_kernel(GemmArgs g, float *partia
       for (int e = 0; e < 16; ++e)
         ct[(wm * WM + i * 32 + (e >> 2) * 8 + g32 * 4 + (e & 3)) * CLD + wn * WN + j * 32 + r32] = acc[i][j][e];
   __syncthreads();
+  auto tile_at = [&](int row, int col) {
+    float v = 0.0f;
+#pragma unroll
+    for (int q = 0; q < KG; ++q) v += ((const float *)(lds + q * GROUP_BYTES))[row * CLD + col];
+    return v;
+  };
+  constexpr int NT = 256 * KG;
+  if (SPLIT) {
+    float *P = partial + (size_t)blockIdx.z * g.M * g.N;
+    for (int idx = tid; idx < BM * BN / 4; idx += NT) {
+      const int row = idx / (BN / 4), c4 = (idx % (BN / 4)) * 4;
+      const int m = m0 + row;
+      if (m >= g.M) continue;
+      f32x4 v;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] = tile_at(row, c4 + q);
+      *(f32x4 *)(P + (size_t)m * g.N + n0 + c4) = v;
+    }
+    return;
+  }
   const int tile_part = (EPI == EPI_QKV || EPI == EPI_TEXTKV) ? n0 / g.hidden : 0;
   const bool transposed = (EPI == EPI_QKV && tile_part == 2) || (EPI == EPI_TEXTKV && tile_part == 1);
   if (!transposed) {
-#pragma unroll
-    for (int k = 0; k < BM * BN / 4 / 256; ++k) {
-      const int idx = tid + k * 256, row = idx / (BN / 4), c4 = (idx % (BN / 4)) * 4;
+    for (int idx = tid; idx < BM * BN / 4; idx += NT) {
+      const int row = idx / (BN / 4), c4 = (idx % (BN / 4)) * 4;
       const int m = m0 + row;
       if (m >= g.M) continue;
       const int n = n0 + c4;
       const f32x4 bb = g.bias ? *(const f32x4 *)(g.bias + n) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
       float v[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) v[q] = ct[row * CLD + c4 + q] + bb[q];
+      for (int q = 0; q < 4; ++q) v[q] = tile_at(row, c4 + q) + bb[q];
       epi4<EPI>(g, m, n, v, tile_part);
     }
   } else {
-#pragma unroll
-    for (int k = 0; k < BM * BN / 4 / 256; ++k) {
-      const int idx = tid + k * 256, col = idx / (BM / 4), r4 = (idx % (BM / 4)) * 4;
+    for (int idx = tid; idx < BM * BN / 4; idx += NT) {
+      const int col = idx / (BM / 4), r4 = (idx % (BM / 4)) * 4;
       const int n = n0 + col;
       const float bn = g.bias ? g.bias[n] : 0.0f;
       const int c = n - tile_part * g.hidden, hh = c / kHeadDim, dd = c - hh * kHeadDim;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int m = m0 + r4 + q;
-        if (m < g.M) epi_store<EPI>(g, m, n, ct[(r4 + q) * CLD + col] + bn, 1.0f, tile_part, hh, dd);
+        if (m < g.M) epi_store<EPI>(g, m, n, tile_at(r4 + q, col) + bn, 1.0f, tile_part, hh, dd);
       }
     }
   }
+  (void)t4;
 }
 
 // Sum of the split partials in split order, then the epilogue.  One thread
@@ -332,11 +339,12 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs g, const fl
   epi_store<EPI>(g, m, n, v + bn, gate, part, hh, dd);
 }
 
-template <int BM, int BN, int STAGES, bool SPLIT>
+template <int BM, int BN, int STAGES, int KG, bool SPLIT>
 static void launch_g2(const GemmArgs &a, int epi, int splits, float *partial, hipStream_t s) {
   dim3 grid(a.N / BN, (a.M + BM - 1) / BM, splits);
   const int kps = a.K / splits;
-#define RC_G2(E) hipLaunchKernelGGL((gemm2_kernel<BM, BN, STAGES, E, SPLIT>), grid, dim3(256), 0, s, a, partial, kps)
+#define RC_G2(E) \
+  hipLaunchKernelGGL((gemm2_kernel<BM, BN, STAGES, KG, E, SPLIT>), grid, dim3(256 * KG), 0, s, a, partial, kps)
   switch (epi) {
     case EPI_STORE: RC_G2(EPI_STORE); break;
     case EPI_GELU: RC_G2(EPI_GELU); break;
@@ -361,25 +369,32 @@ static void launch_reduce(const GemmArgs &a, int epi, int splits, const float *p
 #undef RC_RD
 }
 
-// Choice of tile and split count for a shape.  Measured on the step's shapes
-// (723 and 4096 rows, N in {1152, 3456, 4608}, K in {1152, 4608}): 64x128
-// tiles beat 128x128 everywhere but one shape (within 4 %), and split-K only
-// pays for K = 4608 when the grid is short of workgroups (the partial sums and
-// their reduction cost more than the idle CUs otherwise).
+// Choice of tile, K groups and split count for a shape (measured on the
+// step's shapes with cold weights: 723 and 4096 rows, N in {1152, 3456,
+// 4608}, K in {1152, 4608}).  64x128 tiles throughout.  When the grid has few
+// tiles (the N = 1152 GEMMs at a few hundred rows) a workgroup runs two K
+// groups of four waves, which doubles the waves per CU without global
+// partials; split-K over the grid only pays for K = 4608 with few tiles.
 GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats) {
-  GemmPlan p{64, 128, 1};
+  GemmPlan p{64, 128, 1, 1};
   const long tiles = (long)((M + 63) / 64) * (N / 128);
   const int nk = K / G2_BK;
-  if (K >= 2048 && tiles < 384 && nk % 2 == 0 && (size_t)2 * M * N <= partial_cap_floats) p.splits = 2;
+  if (tiles < 160 && nk % 2 == 0) p.kg = 2;
+  if (K >= 2048 && tiles < 384 && nk % (2 * p.kg) == 0 && (size_t)2 * M * N <= partial_cap_floats) p.splits = 2;
   return p;
 }
 
 hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &pl, float *partial, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
-  if (pl.bm != 64 || pl.bn != 128 || a.N % 128 || a.K % (G2_BK * pl.splits)) return hipErrorInvalidValue;
+  if (pl.bm != 64 || pl.bn != 128 || a.N % 128 || a.K % (G2_BK * pl.splits * pl.kg)) return hipErrorInvalidValue;
   const bool split = pl.splits > 1;
-  if (split) launch_g2<64, 128, 3, true>(a, epi, pl.splits, partial, s);
-  else launch_g2<64, 128, 2, false>(a, epi, 1, nullptr, s);
+  if (pl.kg == 2) {
+    if (split) launch_g2<64, 128, 3, 2, true>(a, epi, pl.splits, partial, s);
+    else launch_g2<64, 128, 3, 2, false>(a, epi, 1, nullptr, s);
+  } else {
+    if (split) launch_g2<64, 128, 3, 1, true>(a, epi, pl.splits, partial, s);
+    else launch_g2<64, 128, 2, 1, false>(a, epi, 1, nullptr, s);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !split) return e;
   launch_reduce(a, epi, pl.splits, partial, s);
