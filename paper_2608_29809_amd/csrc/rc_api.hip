@@ -307,7 +307,7 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
     RC_TRY(timed(c, RC_KC_EMBED, s, [&] { return rc::launch_embed<T>(ea, R, s); }));
   }
 
-  // self-attention key splits: fill 3 workgroups x 256 CUs with as few
+  // self-attention key splits: fill 2 workgroups x 256 CUs with as few
   // splits as possible (the bf16 kernel takes uneven splits)
   long qtiles = 0;
   for (int b = 0; b < B; ++b) qtiles += (counts[b] + 127) / 128;
@@ -318,7 +318,7 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
     for (int sp = 1; sp <= max_s; ++sp) {
       if ((long)R * sp > part_cap_rows(R) && sp > 1) break;
       const long wgs = qtiles * H * sp;
-      const double eff = wgs / (std::ceil(wgs / 768.0) * 768.0) - 0.01 * sp;  // 3 workgroups per CU
+      const double eff = wgs / (std::ceil(wgs / 512.0) * 512.0) - 0.01 * sp;  // 2 workgroups per CU
       if (eff > best) { best = eff; splits = sp; }
     }
   } else {

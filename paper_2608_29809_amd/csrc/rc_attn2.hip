@@ -26,6 +26,9 @@
 namespace rc {
 
 constexpr int A2_BQ = 128, A2_BK = 64;
+#ifndef ATT2_STAGES
+#define ATT2_STAGES 2
+#endif
 
 __device__ __forceinline__ int key_perm2(int m) {
   return ((m >> 4) & 1) * 16 + ((m >> 2) & 1) * 8 + ((m >> 3) & 1) * 4 + (m & 3);
@@ -34,21 +37,41 @@ __device__ __forceinline__ int key_perm2(int m) {
 __device__ __forceinline__ void lds_barrier2() { asm volatile("s_barrier" ::: "memory"); }
 __device__ __forceinline__ void wait_vm0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-template <bool CROSS>
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+template <bool CROSS, int STAGES>
 __global__ __launch_bounds__(256, 2) void attn2_kernel(AttnArgs a) {
   constexpr int D = kHeadDim;
   constexpr int KT_BYTES = A2_BK * D * 2;      // 9216: K tile [64][72]
   constexpr int VT_BYTES = D * A2_BK * 2;      // 9216: V^T tile [72][64]
   constexpr int STAGE = KT_BYTES + VT_BYTES;
   constexpr int K_CH = KT_BYTES / 16;          // 576 chunks
-  __shared__ __attribute__((aligned(1024))) char lds[2 * STAGE];
+  __shared__ __attribute__((aligned(1024))) char lds[STAGES * STAGE + 128];
+  // a row of 64 bf16 ones: row 72 of the V^T operand, so that output row 72
+  // of O^T accumulates sum_k P[k] -- the softmax denominator, with the same
+  // rounded probabilities as the numerator
+  char *ones_row = lds + STAGES * STAGE;
+  if (threadIdx.x < 8) *(V16 *)(ones_row + threadIdx.x * 16) = V16{{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u}};
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 5, r32 = lane & 31;
+  // the wave index is uniform across the wave; telling the compiler so keeps
+  // the per-wave load choices on scalar branches
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 5, r32 = lane & 31;
   const int heads = a.hidden / D;
-  const int b = blockIdx.z;
-  const int h = blockIdx.y % heads, split = blockIdx.y / heads;
+  // XCD-aware order: workgroups are dealt to the eight XCDs round-robin, so
+  // consecutive logical ids are packed onto one XCD; the query tiles of one
+  // (chain, head, key range) are consecutive and read their keys and values
+  // through that XCD's L2 instead of each fetching them from HBM.
+  const int G = gridDim.x, Y = gridDim.y, T = G * Y * gridDim.z;
+  const int p = blockIdx.x + G * (blockIdx.y + Y * blockIdx.z);
+  const int L = (T % 8 == 0) ? (p % 8) * (T / 8) + p / 8 : p;
+  const int qt = L % G, hy = (L / G) % Y, b = L / (G * Y);
+  const int h = hy % heads, split = hy / heads;
   const int r0 = a.offsets[b], r1 = a.offsets[b + 1];
-  const int q0 = r0 + blockIdx.x * A2_BQ;
+  const int q0 = r0 + qt * A2_BQ;
   if (q0 >= r1) return;  // uniform across the workgroup
   const int my_q = q0 + wave * 32 + r32;
   const bool q_ok = my_q < r1;
@@ -97,35 +120,49 @@ __global__ __launch_bounds__(256, 2) void attn2_kernel(AttnArgs a) {
   for (int t = 0; t < 3; ++t)
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[t][e] = 0.0f;
-  float m_run = -INFINITY, l_run = 0.0f;
+  float m_run = -INFINITY;
   float sd[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) sd[j] = -INFINITY;
   const float c2 = a.scale_log2;
 
-  if (t_beg < t_end) issue(0, t_beg);
+  // ring of STAGES tiles: tiles t+1 .. t+STAGES-1 are in flight while tile t
+  // is consumed.  Wave 0 issues 6 loads per tile (the 576-chunk K and V
+  // tiles leave 64 chunks each over), the other waves 4.
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (t_beg + s < t_end) issue(s, t_beg + s);
   for (int tile = t_beg; tile < t_end; ++tile) {
-    const int stage = (tile - t_beg) & 1;
-    wait_vm0();
+    const int stage = (tile - t_beg) % STAGES;
+    if (tile + STAGES - 2 < t_end) {
+      if (wave == 0) wait_vm<(STAGES - 2) * 6>();
+      else wait_vm<(STAGES - 2) * 4>();
+    } else {
+      wait_vm0();
+    }
     lds_barrier2();
-    if (tile + 1 < t_end) issue(stage ^ 1, tile + 1);
+    if (tile + STAGES - 1 < t_end) issue((tile - t_beg + STAGES - 1) % STAGES, tile + STAGES - 1);
     const char *ks = lds + stage * STAGE, *vs = ks + KT_BYTES;
     const int key0 = tile * A2_BK;
 
-    f32x16 s[2];
+    // all ten K fragments of the tile are read before the first MFMA
+    bf16x8 kf[2][5];
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
-#pragma unroll
-      for (int e = 0; e < 16; ++e) s[st][e] = 0.0f;
       const char *krow = ks + (st * 32 + key_perm2(r32)) * (D * 2);
 #pragma unroll
-      for (int c = 0; c < 5; ++c) {
-        const int d0 = c * 16 + g * 8;
-        bf16x8 kf = Mfma<bf16>::zero();
-        if (d0 < D) kf = *(const bf16x8 *)(krow + d0 * 2);
-        s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], s[st], 0, 0, 0);
-      }
+      for (int c = 0; c < 5; ++c) kf[st][c] = *(const bf16x8 *)(krow + (c * 16 + g * 8) * 2);
+      // d0 = 72 (c = 4, upper half-wave) lies past the row; it reads the next
+      // row, which meets zero queries, and is then zeroed without a branch
+      // so that no non-finite neighbour can leak
+      kf[st][4] = (g == 0) ? kf[st][4] : Mfma<bf16>::zero();
     }
+    f32x16 s[2];
+#pragma unroll
+    for (int c = 0; c < 5; ++c)
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+        s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st][c], qf[c], c == 0 ? f32x16{} : s[st], 0, 0, 0);
 
     // lane group g, sub-tile st, accumulator e = c*8 + k  <->  key st*32 + c*16 + g*8 + k
     float tmax = -INFINITY;
@@ -154,10 +191,13 @@ __global__ __launch_bounds__(256, 2) void attn2_kernel(AttnArgs a) {
       }
     }
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    // Lazy rescaling: the reference maximum m_run only moves when some query
+    // of the wave gained more than 2^8 over it, so probabilities stay below
+    // 256 and the output rescale is rare.  The result is unchanged: every
+    // probability and the denominator share the reference.
     const float m_new = fmaxf(m_run, tmax);
-    if (__any(m_new > m_run)) {
+    if (__any((m_new - m_run) * c2 > 8.0f)) {
       const float alpha = (m_run == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m_run - m_new) * c2);
-      l_run *= alpha;
 #pragma unroll
       for (int t = 0; t < 3; ++t)
 #pragma unroll
@@ -166,18 +206,13 @@ __global__ __launch_bounds__(256, 2) void attn2_kernel(AttnArgs a) {
     }
     const float mc = (m_run == -INFINITY) ? 0.0f : m_run * c2;
     bf16x8 pf[2][2];
-    float psum = 0.0f;
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int c = 0; c < 2; ++c)
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][c * 8 + k], c2, -mc));
-          psum += p;
-          pf[st][c][k] = (bf16)p;
-        }
-    l_run += psum;
+        for (int k = 0; k < 8; ++k)
+          pf[st][c][k] = (bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[st][c * 8 + k], c2, -mc));
 
 #pragma unroll
     for (int st = 0; st < 2; ++st)
@@ -186,15 +221,19 @@ __global__ __launch_bounds__(256, 2) void attn2_kernel(AttnArgs a) {
         const int lc = st * 4 + c * 2 + g;  // logical 16-byte chunk of the 64-key row
 #pragma unroll
         for (int t = 0; t < 3; ++t) {
-          const int d = t * 32 + r32;
-          bf16x8 vf = Mfma<bf16>::zero();
-          if (d < D) vf = *(const bf16x8 *)(vs + d * 128 + ((lc ^ (d & 7)) << 4));
+          // rows d >= 72 of the V^T operand only feed output rows that are
+          // never stored, so their lanes read a clamped in-bounds row
+          const int d = min(t * 32 + r32, D - 1);
+          const char *va = vs + d * 128 + ((lc ^ (d & 7)) << 4);
+          if (t == 2 && r32 == 8) va = ones_row + (lc << 4);
+          const bf16x8 vf = *(const bf16x8 *)va;
           o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[st][c], o[t], 0, 0, 0);
         }
       }
   }
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  // denominator: output row 72 = accumulator 4 of o[2] in the lower half-wave
+  const float l_tot = __shfl(o[2][4], r32, 64);
   if (CROSS && a.pmaps) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
@@ -244,9 +283,9 @@ hipError_t launch_attention2(const AttnArgs &a, int n_chains, int max_rows, bool
   if (a.n_keys % A2_BK != 0 || a.splits < 1 || a.splits > a.n_keys / A2_BK) return hipErrorInvalidValue;
   dim3 grid((max_rows + A2_BQ - 1) / A2_BQ, (a.hidden / kHeadDim) * a.splits, n_chains);
   if (cross)
-    hipLaunchKernelGGL(attn2_kernel<true>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((attn2_kernel<true, 2>), grid, dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL(attn2_kernel<false>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((attn2_kernel<false, ATT2_STAGES>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
