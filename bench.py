@@ -45,6 +45,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=6, help="layers in the oracle timing sample")
     ap.add_argument("--quick", action="store_true", help="skip the schedule legs (profiling runs)")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay one captured HIP graph per reuse step instead of host launches")
+    ap.add_argument("--copy-calibrate", type=int, default=0, metavar="MIB",
+                    help="only run one plain device-to-device copy of MIB MiB (HBM counter calibration)")
     return ap.parse_args()
 
 
@@ -59,6 +63,15 @@ def main():
               file=sys.stderr)
         sys.exit(2)
     import torch
+    if args.copy_calibrate:
+        n = args.copy_calibrate * (1 << 20) // 4
+        x = torch.ones(n, dtype=torch.float32, device="cuda")
+        y = torch.empty_like(x)
+        torch.cuda.synchronize()
+        y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4}))
+        return
     import synth
     from paper_2608_29809_amd import abi
     from paper_2608_29809_amd.runtime import ActiveSet, RegionCacheModel
@@ -130,7 +143,32 @@ def main():
         return ev0.elapsed_time(ev1) / 1000.0, wall
 
     # ---------------------------------------------------------------- headline: reuse steps
-    t_reuse, wall_reuse = time_loop(reuse, args.steps, args.warmup)
+    # The active set is fixed for the 16 reuse steps of a turn, so every
+    # launch of a reuse step is known after localisation: each step is
+    # captured once into a HIP graph (kernel nodes only) and replayed.
+    t_eager, _ = time_loop(reuse, args.steps, args.warmup)
+    ms_eager = 1000.0 * t_eager / args.steps
+    log(f"reuse step (host launches): {ms_eager:.3f} ms ({args.steps / t_eager:.1f} steps/s)")
+    graphs = None
+    if args.graph:
+        graphs = []
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for k in range(len(reuse_steps)):
+                gr = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(gr, stream=side):
+                    reuse(k)
+                graphs.append(gr)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+
+        def reuse_graph(k):
+            graphs[k % len(graphs)].replay()
+
+        t_reuse, wall_reuse = time_loop(reuse_graph, args.steps, args.warmup)
+    else:
+        t_reuse, wall_reuse = t_eager, 0.0
     ms_reuse = 1000.0 * t_reuse / args.steps
     log(f"reuse step: {ms_reuse:.3f} ms ({args.steps / t_reuse:.1f} steps/s; wall {wall_reuse:.3f}s)")
 
@@ -210,6 +248,15 @@ def main():
                         plan="4 dense (maps at step 3) + localisation + 16 reuse")
         log(f"turn: {t_turn * 1000:.1f} ms vs all-dense {t_turn_dense * 1000:.1f} ms")
 
+    # ---------------------------------------------------------------- localisation workload
+    loc = None
+    sweep = None
+    if not args.quick:
+        loc = localize_leg(args)
+        del cache
+        torch.cuda.empty_cache()
+        sweep = sweep_leg(model, args)
+
     # ---------------------------------------------------------------- oracle on the host cores
     cpu = None
     if not args.no_cpu_baseline:
@@ -233,15 +280,115 @@ def main():
                    "tokens": N, "active_tokens": R, "active_frac": round(R / N, 4), "blobs": n_blobs,
                    "batch": 1, "layers": shape.layers, "sampler_steps": T, "dense_steps": n_dense,
                    "parallelism": "single GPU"},
+        "launch": "hip_graph_per_step" if graphs else "host",
+        "host_launch_ms_per_step": round(ms_eager, 4),
         "dense_step_ms": round(ms_dense, 4),
         "dense_steps_per_s": round(1000.0 / ms_dense, 3),
         "speedup_vs_dense": round(ms_dense / ms_reuse, 3),
         "schedule": schedule,
         "kernels_ms_per_step": {k: round(v["total_ms"], 4) for k, v in per.items()},
         "roofline": roofline,
+        "localize": loc,
+        "fraction_sweep": sweep,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def localize_leg(args):
+    """Edit-region localisation at 1024 px: bf16 logits [28, 16, 4096, 120]
+    (N(0,1), +3 on 6 delta columns over a seeded blob) -> per-token maps ->
+    range-normalised threshold 0.3, union, 3x3 dilation -> mask + indices.
+    The logits pass is HBM-bound; its rate is reported against 8 TB/s."""
+    import torch
+    import synth
+    from paper_2608_29809_amd.runtime import RegionCacheModel, maps_from_logits
+    gh = gw = 64
+    Z, delta, blob = synth.make_logits(28, 16, gh * gw, 120, gh, gw, n_delta=6, seed=args.seed, frac=0.12)
+    Zt = torch.from_numpy(Z).to(torch.bfloat16).cuda()
+    del Z
+    shp = synth.ModelShape(layers=1, grid_h=gh, grid_w=gw, dtype="bf16")
+    m = RegionCacheModel(shp, synth.make_weights(shp, seed=0))
+    for _ in range(2):
+        maps = maps_from_logits(Zt, delta)
+        mask, act = m.localize(maps[None].contiguous(), len(delta), 0.3, 1)
+    torch.cuda.synchronize()
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    reps = 10
+    e0.record()
+    for _ in range(reps):
+        maps = maps_from_logits(Zt, delta)
+    e1.record()
+    for _ in range(reps):
+        mask, act = m.localize(maps[None].contiguous(), len(delta), 0.3, 1)  # includes one host sync
+    e2.record()
+    torch.cuda.synchronize()
+    t_maps = e0.elapsed_time(e1) / reps
+    t_loc = e1.elapsed_time(e2) / reps
+    nbytes = Zt.numel() * 2
+    gbs = nbytes / (t_maps * 1e-3) / 1e9
+    log(f"localisation: maps {t_maps * 1000:.1f} us ({gbs:.0f} GB/s), mask+compaction {t_loc * 1000:.1f} us, "
+        f"{act.total} active tokens")
+    return dict(workload="logits bf16 [28,16,4096,120], 6 delta columns", maps_us=round(t_maps * 1000, 2),
+                logits_gbs=round(gbs, 1), hbm_frac=round(gbs / PEAK_HBM_GBS, 4),
+                mask_and_compaction_us=round(t_loc * 1000, 2), active_tokens=int(act.total))
+
+
+def sweep_leg(model1, args):
+    """Batch-4 active-fraction sweep at 1024 px: four chains, fresh blob masks
+    at 5/10/25/50/100 % of 4096 tokens; reuse-step and dense-step times."""
+    import torch
+    import synth
+    from paper_2608_29809_amd.runtime import ActiveSet
+    shape = synth.shape_c3()
+    B, T = 4, 20
+    tgrid = synth.timestep_grid(T)
+    model = model1
+    cache = model.alloc_cache(B, T)
+    txt = synth.make_text(shape, B, args.seed + 1)
+    tkv = model.prepare_text(model.to_storage(txt))
+    lat = [torch.from_numpy(synth.make_latent(shape, B, args.seed + 1)).cuda()]
+    for s in range(T):
+        lat.append(torch.empty_like(lat[0]))
+        model.build_cache(cache, s, lat[s], int(tgrid[s]), int(tgrid[s + 1]) if s + 1 < T else -1, tkv,
+                          latent_out=lat[s + 1])
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+
+    def timed(fn, n):
+        fn(0)
+        torch.cuda.synchronize()
+        ev[0].record()
+        for k in range(n):
+            fn(k)
+        ev[1].record()
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / n
+
+    out = {}
+    steps = list(range(4, T))
+    for f in (0.05, 0.10, 0.25, 0.50, 1.00):
+        rng = np.random.default_rng([args.seed, int(f * 1000)])
+        per = [np.flatnonzero(synth.blob_mask(64, 64, f, int(rng.integers(1, 4)), rng)) for _ in range(B)]
+        act = ActiveSet.from_lists(per)
+
+        def rs(k, act=act):
+            s = steps[k % len(steps)]
+            model.reuse_step(cache, s, act, lat[s], int(tgrid[s]), int(tgrid[s + 1]) if s + 1 < T else -1, tkv,
+                             latent_out=lat[s + 1])
+
+        out[f"{int(f * 100)}%"] = round(timed(rs, 8), 3)
+    def ds(k):
+        s = steps[k % len(steps)]
+        model.build_cache(cache, s, lat[s], int(tgrid[s]), int(tgrid[s + 1]) if s + 1 < T else -1, tkv,
+                          latent_out=lat[s + 1])
+    dense_ms = round(timed(ds, 4), 3)
+    log("fraction sweep (batch 4, ms per step): " + ", ".join(f"{k} {v}" for k, v in out.items()) +
+        f"; dense {dense_ms}")
+    del cache
+    torch.cuda.empty_cache()
+    return dict(batch=B, reuse_step_ms=out, dense_step_ms=dense_ms,
+                speedup_vs_dense={k: round(dense_ms / v, 3) for k, v in out.items()})
 
 
 def _kernel_hash(cls):

@@ -67,7 +67,7 @@ __global__ __launch_bounds__(256, 2) void attn2_kernel(AttnArgs a) {
   // through that XCD's L2 instead of each fetching them from HBM.
   const int G = gridDim.x, Y = gridDim.y, T = G * Y * gridDim.z;
   const int p = blockIdx.x + G * (blockIdx.y + Y * blockIdx.z);
-  const int L = (T % 8 == 0) ? (p % 8) * (T / 8) + p / 8 : p;
+  const int L = xcd_logical_id(p, T);
   const int qt = L % G, hy = (L / G) % Y, b = L / (G * Y);
   const int h = hy % heads, split = hy / heads;
   const int r0 = a.offsets[b], r1 = a.offsets[b + 1];

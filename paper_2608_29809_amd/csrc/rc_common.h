@@ -74,6 +74,18 @@ __device__ __forceinline__ float gelu_tanh(float x) {
 }
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + __expf(-x)); }
 
+// XCD-aware renumbering of a grid.  Workgroups are dealt to the eight XCDs
+// round-robin by linear id p, so XCD x runs p = x, x+8, x+16, ...  The
+// logical id returned packs each XCD's workgroups into one contiguous range
+// (XCD x gets [off_x, off_x + count_x)), so that logically adjacent work --
+// which the caller arranges to share operands -- shares that XCD's L2.  A
+// bijection on [0, T) for any T.
+__device__ __forceinline__ int xcd_logical_id(int p, int T) {
+  const int x = p & 7, q = T >> 3, rem = T & 7;
+  const int off = x * q + min(x, rem);
+  return off + (p >> 3);
+}
+
 // Row r of the active set is packed as (chain << 16) | token.
 __device__ __forceinline__ int row_chain(int packed) { return packed >> 16; }
 __device__ __forceinline__ int row_token(int packed) { return packed & 0xFFFF; }

@@ -153,11 +153,13 @@ __device__ __forceinline__ void col_info(const GemmArgs &g, int n, float &bn, fl
   }
 }
 
-template <int BM, int BN, int STAGES, int KG, int EPI, bool SPLIT>
-__global__ __launch_bounds__(256 * KG) void gemm2_kernel(GemmArgs g, float *partial, int k_per_split) {
-  constexpr int WM = BM / 2, WN = BN / 2, FM = WM / 32, FN = WN / 32;
-  constexpr int A_LD = BM * 8 / 256;  // direct loads per thread per stage (16 bytes each)
-  constexpr int B_LD = BN * 8 / 256;
+template <int BM, int BN, int STAGES, int KG, int WGM, int WGN, int EPI, bool SPLIT>
+__global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, float *partial, int k_per_split) {
+  constexpr int NW = WGM * WGN;                       // waves per K group
+  constexpr int WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32;
+  constexpr int A_LD = BM * 8 / (64 * NW);            // direct loads per thread per stage (16 bytes each)
+  constexpr int B_LD = BN * 8 / (64 * NW);
+  static_assert(A_LD * 64 * NW == BM * 8 && B_LD * 64 * NW == BN * 8, "tile rows must split over the waves");
   constexpr int LPS = A_LD + B_LD;
   constexpr int STAGE_BYTES = (BM + BN) * 128;
   constexpr int GROUP_BYTES = STAGES * STAGE_BYTES;  // one K group's ring
@@ -165,21 +167,27 @@ __global__ __launch_bounds__(256 * KG) void gemm2_kernel(GemmArgs g, float *part
   static_assert(BM * CLD * 4 <= GROUP_BYTES, "output tile must fit a group's ring");
   __shared__ __attribute__((aligned(1024))) char lds[KG * GROUP_BYTES];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int kgrp = wave >> 2, w4 = wave & 3, t4 = tid & 255;
-  const int wm = w4 >> 1, wn = w4 & 1;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kgrp = wave / NW, w4 = wave % NW;
+  const int wm = w4 / WGN, wn = w4 % WGN;
 
   // XCD-aware tile order: logical tile L walks the row tiles of one column
   // panel before moving to the next panel; physical id p runs on XCD p % 8.
-  const int tiles_m = gridDim.y, tiles_n = gridDim.x, T = tiles_m * tiles_n;
-  const int p = blockIdx.y * tiles_n + blockIdx.x;
-  int L = p;
-  if (T % 8 == 0) L = (p % 8) * (T / 8) + p / 8;
-  const int tn = L / tiles_m, tm = L - (L / tiles_m) * tiles_m;
+  // Logical order per split: groups of up to 16 row tiles, and within a
+  // group row tiles fastest, then column panels.  Consecutive logical tiles
+  // run on one XCD, so the ~64 tiles in flight there share <= 16 row panels
+  // of A and a few column panels of W in that XCD's L2.
+  const int tiles_m = gridDim.y, tiles_n = gridDim.x, TT = tiles_m * tiles_n, T = TT * gridDim.z;
+  const int p = blockIdx.x + tiles_n * (blockIdx.y + tiles_m * blockIdx.z);
+  const int L = xcd_logical_id(p, T);
+  const int kz = L / TT, r = L - kz * TT;
+  constexpr int GM = 16;
+  const int grp = r / (GM * tiles_n), gm = min(GM, tiles_m - grp * GM), idx = r - grp * GM * tiles_n;
+  const int tm = grp * GM + idx % gm, tn = idx / gm;
   const int m0 = tm * BM, n0 = tn * BN;
   // K group kgrp covers its own contiguous share of this split's K range
   const int kps_g = k_per_split / KG;
-  const int kbeg = blockIdx.z * k_per_split + kgrp * kps_g;
+  const int kbeg = kz * k_per_split + kgrp * kps_g;
   const int nk = kps_g / G2_BK;
   char *ring = lds + kgrp * GROUP_BYTES;
 
@@ -191,20 +199,20 @@ __global__ __launch_bounds__(256 * KG) void gemm2_kernel(GemmArgs g, float *part
     char *sb = sa + BM * 128;
 #pragma unroll
     for (int i = 0; i < A_LD; ++i) {
-      const int ch = (i * 4 + w4) * 64 + lane;
+      const int ch = (i * NW + w4) * 64 + lane;
       const int r = ch >> 3, c = (ch & 7) ^ (r & 7);
       const int gr = min(m0 + r, g.M - 1);
       const bf16 *src = A + (size_t)gr * g.lda + k0 + c * 8;
       __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
-                                       (__attribute__((address_space(3))) void *)(sa + (i * 4 + w4) * 1024), 16, 0, 0);
+                                       (__attribute__((address_space(3))) void *)(sa + (i * NW + w4) * 1024), 16, 0, 0);
     }
 #pragma unroll
     for (int i = 0; i < B_LD; ++i) {
-      const int ch = (i * 4 + w4) * 64 + lane;
+      const int ch = (i * NW + w4) * 64 + lane;
       const int r = ch >> 3, c = (ch & 7) ^ (r & 7);
       const bf16 *src = W + (size_t)(n0 + r) * g.K + k0 + c * 8;
       __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
-                                       (__attribute__((address_space(3))) void *)(sb + (i * 4 + w4) * 1024), 16, 0, 0);
+                                       (__attribute__((address_space(3))) void *)(sb + (i * NW + w4) * 1024), 16, 0, 0);
     }
   };
 
@@ -280,9 +288,9 @@ __global__ __launch_bounds__(256 * KG) void gemm2_kernel(GemmArgs g, float *part
     for (int q = 0; q < KG; ++q) v += ((const float *)(lds + q * GROUP_BYTES))[row * CLD + col];
     return v;
   };
-  constexpr int NT = 256 * KG;
+  constexpr int NT = 64 * NW * KG;
   if (SPLIT) {
-    float *P = partial + (size_t)blockIdx.z * g.M * g.N;
+    float *P = partial + (size_t)kz * g.M * g.N;
     for (int idx = tid; idx < BM * BN / 4; idx += NT) {
       const int row = idx / (BN / 4), c4 = (idx % (BN / 4)) * 4;
       const int m = m0 + row;
@@ -321,7 +329,6 @@ __global__ __launch_bounds__(256 * KG) void gemm2_kernel(GemmArgs g, float *part
       }
     }
   }
-  (void)t4;
 }
 
 // Sum of the split partials in split order, then the epilogue.  One thread
@@ -339,12 +346,13 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs g, const fl
   epi_store<EPI>(g, m, n, v + bn, gate, part, hh, dd);
 }
 
-template <int BM, int BN, int STAGES, int KG, bool SPLIT>
+template <int BM, int BN, int STAGES, int KG, int WGM, int WGN, bool SPLIT>
 static void launch_g2(const GemmArgs &a, int epi, int splits, float *partial, hipStream_t s) {
   dim3 grid(a.N / BN, (a.M + BM - 1) / BM, splits);
   const int kps = a.K / splits;
-#define RC_G2(E) \
-  hipLaunchKernelGGL((gemm2_kernel<BM, BN, STAGES, KG, E, SPLIT>), grid, dim3(256 * KG), 0, s, a, partial, kps)
+#define RC_G2(E)                                                                                       \
+  hipLaunchKernelGGL((gemm2_kernel<BM, BN, STAGES, KG, WGM, WGN, E, SPLIT>), grid, dim3(64 * WGM * WGN * KG), 0, s, \
+                     a, partial, kps)
   switch (epi) {
     case EPI_STORE: RC_G2(EPI_STORE); break;
     case EPI_GELU: RC_G2(EPI_GELU); break;
@@ -376,7 +384,7 @@ static void launch_reduce(const GemmArgs &a, int epi, int splits, const float *p
 // groups of four waves, which doubles the waves per CU without global
 // partials; split-K over the grid only pays for K = 4608 with few tiles.
 GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats) {
-  GemmPlan p{64, 128, 1, 1};
+  GemmPlan p{64, 128, 1, 1, 4};
   const long tiles = (long)((M + 63) / 64) * (N / 128);
   const int nk = K / G2_BK;
   if (tiles < 160 && nk % 2 == 0) p.kg = 2;
@@ -388,13 +396,18 @@ hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &pl, float *p
   if (a.M <= 0) return hipSuccess;
   if (pl.bm != 64 || pl.bn != 128 || a.N % 128 || a.K % (G2_BK * pl.splits * pl.kg)) return hipErrorInvalidValue;
   const bool split = pl.splits > 1;
-  if (pl.kg == 2) {
-    if (split) launch_g2<64, 128, 3, 2, true>(a, epi, pl.splits, partial, s);
-    else launch_g2<64, 128, 3, 2, false>(a, epi, 1, nullptr, s);
+  // wave layouts: 4 = 2x2 waves of 32x64, 2 = 1x2 waves of 64x64, 1 = one wave of 64x128
+#define RC_G2_KG(KGV, STG, WM_, WN_)                                   \
+  if (split) launch_g2<64, 128, STG, KGV, WM_, WN_, true>(a, epi, pl.splits, partial, s); \
+  else launch_g2<64, 128, STG, KGV, WM_, WN_, false>(a, epi, 1, nullptr, s);
+  if (pl.waves == 4) {
+    if (pl.kg == 2) { RC_G2_KG(2, 3, 2, 2) } else { RC_G2_KG(1, 2, 2, 2) }
+  } else if (pl.waves == 2) {
+    if (pl.kg == 2) { RC_G2_KG(2, 3, 1, 2) } else { RC_G2_KG(1, 2, 1, 2) }
   } else {
-    if (split) launch_g2<64, 128, 3, 1, true>(a, epi, pl.splits, partial, s);
-    else launch_g2<64, 128, 2, 1, false>(a, epi, 1, nullptr, s);
+    if (pl.kg == 2) { RC_G2_KG(2, 3, 1, 1) } else { RC_G2_KG(1, 2, 1, 1) }
   }
+#undef RC_G2_KG
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !split) return e;
   launch_reduce(a, epi, pl.splits, partial, s);

@@ -69,7 +69,8 @@ template <typename T> hipError_t launch_gemm(const GemmArgs &a, int epi, hipStre
 
 // bf16 GEMM with direct-to-LDS staging and optional split-K (rc_gemm2.hip).
 struct GemmPlan {
-  int bm, bn, splits, kg;  // kg: K groups inside one workgroup (256 threads each)
+  int bm, bn, splits, kg;  // kg: K groups inside one workgroup
+  int waves;               // waves per K group: 4 (32x64 each), 2 (64x64) or 1 (64x128)
 };
 GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats);
 hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &plan, float *partial, hipStream_t s);
