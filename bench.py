@@ -200,19 +200,13 @@ def main():
         "gemm_qkv": 2.0 * R * 3 * C * C,
         "gemm_fc1": 2.0 * R * F * C,
         "gemm_fc2": 2.0 * R * C * F,
-        "gemm": 2.0 * R * C * C,
+        "gemm_proj": 2.0 * R * C * C,
+        "gemm_xq": 2.0 * R * C * C,
+        "gemm_xproj": 2.0 * R * C * C,
     }
     dom = max((k for k in per if k in flops_per_launch), key=lambda k: per[k]["total_ms"])
     achieved = flops_per_launch[dom] / (per[dom]["avg_us"] * 1e-6) / 1e12
-    traffic = None
-    tpath = os.path.join(ROOT, "profiles", f"traffic_{dom}.json")
-    if os.path.exists(tpath):
-        try:
-            tj = json.load(open(tpath))
-            if tj.get("R") == R and tj.get("source_hash") == _kernel_hash(dom):
-                traffic = tj.get("bytes_per_launch")
-        except Exception:
-            traffic = None
+    traffic = _committed_traffic(dom, R)
     roofline = dict(bound="mfma", kernel=dom, achieved=round(achieved, 2), peak=PEAK_BF16_TFLOPS,
                     unit="TFLOP/s", frac=round(achieved / PEAK_BF16_TFLOPS, 4), traffic=traffic,
                     flops_per_launch=flops_per_launch[dom], avg_launch_us=round(per[dom]["avg_us"], 3))
@@ -391,11 +385,38 @@ def sweep_leg(model1, args):
                 speedup_vs_dense={k: round(dense_ms / v, 3) for k, v in out.items()})
 
 
-def _kernel_hash(cls):
+KERNEL_SOURCES = {  # sources whose text fixes a kernel class's code
+    "attn": ["rc_attn2.hip", "rc_common.h", "rc_internal.h"],
+    "gemm": ["rc_gemm2.hip", "rc_common.h", "rc_internal.h"],
+}
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "hbm_traffic_reuse_step_1024px.md")
+
+
+def kernel_source_hash(cls):
     import hashlib
-    f = {"attn_self": "rc_attn.hip", "attn_cross": "rc_attn.hip"}.get(cls, "rc_gemm.hip")
-    p = os.path.join(ROOT, "paper_2608_29809_amd", "csrc", f)
-    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES["attn" if cls.startswith("attn") else "gemm"]:
+        h.update(open(os.path.join(ROOT, "paper_2608_29809_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def _committed_traffic(cls, R):
+    """HBM bytes per launch of a kernel class from the committed counter
+    summary (FETCH_SIZE and WRITE_SIZE runs, scaled by a plain copy's
+    counts), or None when there is none for this class and active-row count
+    or the kernel's sources have changed since the counters were taken."""
+    if not os.path.exists(TRAFFIC_SUMMARY):
+        return None
+    for line in open(TRAFFIC_SUMMARY):
+        if not line.startswith("traffic-record: "):
+            continue
+        try:
+            rec = json.loads(line[len("traffic-record: "):])
+        except ValueError:
+            continue
+        if rec.get("kernel") == cls and rec.get("R") == R and rec.get("source_hash") == kernel_source_hash(cls):
+            return rec.get("bytes_per_launch")
+    return None
 
 
 def cpu_baseline(shape, W, idx, args):

@@ -283,7 +283,8 @@ rc_status rc_sync(void *stream);
 enum {
   RC_KC_GEMM = 0, RC_KC_ATTN_SELF = 1, RC_KC_ATTN_CROSS = 2, RC_KC_ATTN_COMBINE = 3,
   RC_KC_NORM = 4, RC_KC_EMBED = 5, RC_KC_FINAL = 6, RC_KC_COND = 7, RC_KC_MISC = 8,
-  RC_KC_GEMM_QKV = 9, RC_KC_GEMM_FC1 = 10, RC_KC_GEMM_FC2 = 11, RC_KC_COUNT = 12
+  RC_KC_GEMM_QKV = 9, RC_KC_GEMM_FC1 = 10, RC_KC_GEMM_FC2 = 11, RC_KC_GEMM_PROJ = 12,
+  RC_KC_GEMM_XQ = 13, RC_KC_GEMM_XPROJ = 14, RC_KC_COUNT = 15
 };
 rc_status rc_set_kernel_timing(rc_ctx *ctx, int32_t enable);
 rc_status rc_get_kernel_timing(rc_ctx *ctx, int32_t kernel_class, double *total_ms, int64_t *launches);

@@ -20,10 +20,12 @@ STATUS = {0: "RC_OK", -1: "RC_ERR_INVALID_ARG", -2: "RC_ERR_SHAPE", -3: "RC_ERR_
 RC_F32, RC_BF16 = 0, 1
 RC_FUSE_UPDATE = 1
 (RC_KC_GEMM, RC_KC_ATTN_SELF, RC_KC_ATTN_CROSS, RC_KC_ATTN_COMBINE, RC_KC_NORM, RC_KC_EMBED,
- RC_KC_FINAL, RC_KC_COND, RC_KC_MISC, RC_KC_GEMM_QKV, RC_KC_GEMM_FC1, RC_KC_GEMM_FC2) = range(12)
-RC_KC_COUNT = 12
+ RC_KC_FINAL, RC_KC_COND, RC_KC_MISC, RC_KC_GEMM_QKV, RC_KC_GEMM_FC1, RC_KC_GEMM_FC2, RC_KC_GEMM_PROJ,
+ RC_KC_GEMM_XQ, RC_KC_GEMM_XPROJ) = range(15)
+RC_KC_COUNT = 15
 KERNEL_CLASSES = ["gemm", "attn_self", "attn_cross", "attn_combine", "norm", "embed", "final",
-                  "cond", "misc", "gemm_qkv", "gemm_fc1", "gemm_fc2"]
+                  "cond", "misc", "gemm_qkv", "gemm_fc1", "gemm_fc2", "gemm_proj",
+                  "gemm_xq", "gemm_xproj"]
 
 
 class RcError(RuntimeError):

@@ -14,9 +14,17 @@
 #include "../../include/regioncache.h"
 #include "rc_common.h"
 #include "rc_elem.h"
+#include "rc_launch.h"
 #include "rc_internal.h"
 
 using rc::bf16;
+
+namespace rc {
+LaunchTiming &launch_timing() {
+  static thread_local LaunchTiming t;
+  return t;
+}
+}  // namespace rc
 
 namespace {
 
@@ -140,11 +148,19 @@ template <typename F> rc_status timed(rc_ctx *c, int cls, hipStream_t s, F &&lau
       c->pool.push_back(e);
     }
   }
-  hipEvent_t a = c->pool[c->pool_used++], b = c->pool[c->pool_used++];
-  RC_HIP(hipEventRecord(a, s));
-  RC_HIP(launch());
-  RC_HIP(hipEventRecord(b, s));
-  c->recs.push_back({cls, a, b});
+  // the dispatches stamp the pair themselves: start of the first kernel of
+  // the operation, end of its last kernel
+  hipEvent_t a = c->pool[c->pool_used], b = c->pool[c->pool_used + 1];
+  ::rc::LaunchTiming &lt = ::rc::launch_timing();
+  lt = ::rc::LaunchTiming{a, b, 0};
+  const hipError_t e = launch();
+  const int n = lt.launches;
+  lt = ::rc::LaunchTiming{};
+  RC_HIP(e);
+  if (n > 0) {
+    c->pool_used += 2;
+    c->recs.push_back({cls, a, b});
+  }
   return RC_OK;
 }
 
@@ -206,10 +222,12 @@ double alpha_bar(int t) {
 // One GEMM of the step: bf16 goes through the direct-to-LDS kernel with a
 // per-shape tile/split plan, fp32 through the register-staged kernel.
 template <typename T>
-rc_status gemm(rc_ctx *c, int cls, const rc::GemmArgs &g, int epi, float *part, size_t part_floats, hipStream_t s) {
+rc_status gemm(rc_ctx *c, int cls, const rc::GemmArgs &g, int epi, float *part, size_t part_floats, hipStream_t s,
+               const rc::LnNext *ln = nullptr, bool *ln_done = nullptr) {
+  if (ln_done) *ln_done = false;
   if constexpr (sizeof(T) == 2) {
     const rc::GemmPlan pl = rc::plan_gemm2(g.M, g.N, g.K, part ? part_floats : 0);
-    return timed(c, cls, s, [&] { return rc::launch_gemm2(g, epi, pl, part, s); });
+    return timed(c, cls, s, [&] { return rc::launch_gemm2(g, epi, pl, part, s, ln, ln_done); });
   } else {
     return timed(c, cls, s, [&] { return rc::launch_gemm<T>(g, epi, s); });
   }
@@ -332,12 +350,15 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
   const size_t kv_half = (size_t)H * N * rc::kHeadDim;
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)rc::kHeadDim));
 
+  bool a1_ready = false;  // the previous block's MLP reduction already wrote this block's LN1 rows
   for (int l = 0; l < L; ++l) {
     const rc_layer_weights &lw = c->layers[l];
     T *slot = (T *)(cb + slot_offset(c, T_, 0, step, l));
     T *Ks = slot, *Vts = slot + kv_half, *Hs = slot + 2 * kv_half;
 
-    RC_TRY(timed(c, RC_KC_NORM, s, [&] { return rc::launch_ln_mod<T>(X, R, C, lw.sst, t0, 0, c->cfg.ln_eps, A1, s); }));
+    if (!a1_ready)
+      RC_TRY(timed(c, RC_KC_NORM, s, [&] { return rc::launch_ln_mod<T>(X, R, C, lw.sst, t0, 0, c->cfg.ln_eps, A1, s); }));
+    a1_ready = false;
     {  // QKV with the K/V scatter into the slot
       rc::GemmArgs g{};
       g.A = A1; g.W = lw.qkv_w; g.bias = lw.qkv_b; g.M = R; g.N = 3 * C; g.K = C; g.lda = C;
@@ -363,12 +384,12 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       rc::GemmArgs g{};
       g.A = O; g.W = lw.proj_w; g.bias = lw.proj_b; g.M = R; g.N = C; g.K = C; g.lda = C;
       g.X = X; g.ldx = C; g.gate = lw.sst + 2 * C; g.gate2 = t0 + 2 * C; g.xt = A1;
-      RC_TRY(gemm<T>(c, RC_KC_GEMM, g, rc::EPI_RESID, gpart, gpf, s));
+      RC_TRY(gemm<T>(c, RC_KC_GEMM_PROJ, g, rc::EPI_RESID, gpart, gpf, s));
     }
     {  // cross-attention query
       rc::GemmArgs g{};
       g.A = A1; g.W = lw.xq_w; g.bias = lw.xq_b; g.M = R; g.N = C; g.K = C; g.lda = C; g.out = Q; g.ldo = C;
-      RC_TRY(gemm<T>(c, RC_KC_GEMM, g, rc::EPI_STORE, gpart, gpf, s));
+      RC_TRY(gemm<T>(c, RC_KC_GEMM_XQ, g, rc::EPI_STORE, gpart, gpf, s));
     }
     {  // cross-attention to the text, emitting the delta-token maps
       const T *tkv = (const T *)io->text_kv + (size_t)l * B * text_kv_elems_per_entry(c);
@@ -395,7 +416,7 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       rc::GemmArgs g{};
       g.A = O; g.W = lw.xproj_w; g.bias = lw.xproj_b; g.M = R; g.N = C; g.K = C; g.lda = C;
       g.X = X; g.ldx = C;
-      RC_TRY(gemm<T>(c, RC_KC_GEMM, g, rc::EPI_RESID, gpart, gpf, s));
+      RC_TRY(gemm<T>(c, RC_KC_GEMM_XPROJ, g, rc::EPI_RESID, gpart, gpf, s));
     }
     RC_TRY(timed(c, RC_KC_NORM, s, [&] { return rc::launch_ln_mod<T>(X, R, C, lw.sst, t0, 3, c->cfg.ln_eps, A1, s); }));
     {  // MLP up + GELU
@@ -410,7 +431,12 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       g.rows = rows; g.hidden = C; g.chain_stride = slot_chain_stride;
       if (dense || fuse) g.hslot = Hs;
       else g.hrows = (T *)active_hidden + (size_t)l * R * C;
-      RC_TRY(gemm<T>(c, RC_KC_GEMM_FC2, g, rc::EPI_RESID, gpart, gpf, s));
+      if (l + 1 < L) {
+        const rc::LnNext ln{c->layers[l + 1].sst, t0, 0, c->cfg.ln_eps, A1};
+        RC_TRY(gemm<T>(c, RC_KC_GEMM_FC2, g, rc::EPI_RESID, gpart, gpf, s, &ln, &a1_ready));
+      } else {
+        RC_TRY(gemm<T>(c, RC_KC_GEMM_FC2, g, rc::EPI_RESID, gpart, gpf, s));
+      }
     }
   }
 

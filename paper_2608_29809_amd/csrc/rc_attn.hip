@@ -20,6 +20,7 @@
 // same reason.  Softmax runs in the exp2 domain with the 1/sqrt(72) scale
 // folded into one multiply.
 #include "rc_common.h"
+#include "rc_launch.h"
 #include "rc_internal.h"
 
 namespace rc {
@@ -276,17 +277,30 @@ __global__ void attn_combine_kernel(const float *Opart, const float *ML, T *O, i
   const int r = idx / (heads * G);
   const int rem = idx - (long)r * heads * G;
   const int h = rem / G, d = (rem - h * G) * 4;
-  float M = -INFINITY;
-  for (int s = 0; s < splits; ++s) M = fmaxf(M, ML[(((size_t)s * R + r) * heads + h) * 2]);
-  float num[4] = {0.0f, 0.0f, 0.0f, 0.0f}, den = 0.0f;
-  for (int s = 0; s < splits; ++s) {
-    const float *ml = ML + (((size_t)s * R + r) * heads + h) * 2;
-    const float w = exp2f(ml[0] - M);
-    const f32x4 p = *(const f32x4 *)(Opart + ((size_t)s * R + r) * C + h * kHeadDim + d);
+  // all loads are issued before any use (the split loops are unrolled to the
+  // largest split count and predicated), so a thread waits on memory once
+  constexpr int SMAX = 16;
+  float2 ml[SMAX];
+  f32x4 p[SMAX];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) num[k] += w * p[k];
-    den += w * ml[1];
-  }
+  for (int s = 0; s < SMAX; ++s)
+    if (s < splits) {
+      ml[s] = *(const float2 *)(ML + (((size_t)s * R + r) * heads + h) * 2);
+      p[s] = *(const f32x4 *)(Opart + ((size_t)s * R + r) * C + h * kHeadDim + d);
+    }
+  float M = -INFINITY;
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s)
+    if (s < splits) M = fmaxf(M, ml[s].x);
+  float num[4] = {0.0f, 0.0f, 0.0f, 0.0f}, den = 0.0f;
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s)
+    if (s < splits) {
+      const float w = exp2f(ml[s].x - M);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) num[k] += w * p[s][k];
+      den += w * ml[s].y;
+    }
   const float inv = 1.0f / den;
   float v[4];
 #pragma unroll
@@ -313,9 +327,9 @@ hipError_t launch_attention(const AttnArgs &a, int n_chains, int max_rows, bool 
   if (a.n_keys % ATT_BK != 0 || (a.n_keys / a.splits) % ATT_BK != 0) return hipErrorInvalidValue;
   dim3 grid((max_rows + ATT_BQ - 1) / ATT_BQ, (a.hidden / kHeadDim) * a.splits, n_chains);
   if (emit_maps)
-    hipLaunchKernelGGL((attn_kernel<T, true>), grid, dim3(256), 0, s, a);
+    rc_launch(attn_kernel<T, true>, grid, dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL((attn_kernel<T, false>), grid, dim3(256), 0, s, a);
+    rc_launch(attn_kernel<T, false>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -325,12 +339,13 @@ template hipError_t launch_attention<float>(const AttnArgs &, int, int, bool, hi
 hipError_t launch_attn_combine(const float *Opart, const float *ML, void *O, bool bf16_out, int R,
                                int heads, int splits, hipStream_t s) {
   if (R <= 0) return hipSuccess;
+  if (splits < 1 || splits > 16) return hipErrorInvalidValue;
   const long n = (long)R * heads * (kHeadDim / 4);
   dim3 grid((n + 255) / 256);
   if (bf16_out)
-    hipLaunchKernelGGL(attn_combine_kernel<bf16>, grid, dim3(256), 0, s, Opart, ML, (bf16 *)O, R, heads, splits);
+    rc_launch(attn_combine_kernel<bf16>, grid, dim3(256), 0, s, Opart, ML, (bf16 *)O, R, heads, splits);
   else
-    hipLaunchKernelGGL(attn_combine_kernel<float>, grid, dim3(256), 0, s, Opart, ML, (float *)O, R, heads, splits);
+    rc_launch(attn_combine_kernel<float>, grid, dim3(256), 0, s, Opart, ML, (float *)O, R, heads, splits);
   return hipGetLastError();
 }
 
@@ -338,7 +353,7 @@ hipError_t launch_maps_reduce(const float *pmaps, const int *rows, float *maps, 
                               int n_delta, int tokens, hipStream_t s) {
   if (R <= 0 || n_delta <= 0) return hipSuccess;
   dim3 grid((R * n_delta + 255) / 256);
-  hipLaunchKernelGGL(maps_reduce_kernel, grid, dim3(256), 0, s, pmaps, rows, maps, R, heads, n_delta, tokens);
+  rc_launch(maps_reduce_kernel, grid, dim3(256), 0, s, pmaps, rows, maps, R, heads, n_delta, tokens);
   return hipGetLastError();
 }
 

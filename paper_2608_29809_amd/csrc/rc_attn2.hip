@@ -21,6 +21,7 @@
 // * Key ranges split unevenly over grid.y so the grid fills the chip; the
 //   deterministic combine is rc_attn.hip's.
 #include "rc_common.h"
+#include "rc_launch.h"
 #include "rc_internal.h"
 
 namespace rc {
@@ -283,9 +284,9 @@ hipError_t launch_attention2(const AttnArgs &a, int n_chains, int max_rows, bool
   if (a.n_keys % A2_BK != 0 || a.splits < 1 || a.splits > a.n_keys / A2_BK) return hipErrorInvalidValue;
   dim3 grid((max_rows + A2_BQ - 1) / A2_BQ, (a.hidden / kHeadDim) * a.splits, n_chains);
   if (cross)
-    hipLaunchKernelGGL((attn2_kernel<true, 2>), grid, dim3(256), 0, s, a);
+    rc_launch(attn2_kernel<true, 2>, grid, dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL((attn2_kernel<false, ATT2_STAGES>), grid, dim3(256), 0, s, a);
+    rc_launch(attn2_kernel<false, ATT2_STAGES>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

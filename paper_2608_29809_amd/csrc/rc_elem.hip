@@ -3,6 +3,7 @@
 // conditioning GEMVs, the final layer fused with the DDIM update, and the
 // cache copies of the reuse path.
 #include "rc_common.h"
+#include "rc_launch.h"
 #include "rc_elem.h"
 
 namespace rc {
@@ -20,7 +21,7 @@ __global__ void build_rows_kernel(const int *offsets, const int *idx, int B, int
 
 hipError_t launch_build_rows(const int *offsets, const int *idx, int B, int R, int *rows, hipStream_t s) {
   if (R <= 0) return hipSuccess;
-  hipLaunchKernelGGL(build_rows_kernel, dim3((R + 255) / 256), dim3(256), 0, s, offsets, idx, B, R, rows);
+  rc_launch(build_rows_kernel, dim3((R + 255) / 256), dim3(256), 0, s, offsets, idx, B, R, rows);
   return hipGetLastError();
 }
 
@@ -31,7 +32,7 @@ __global__ void dense_offsets_kernel(int *offsets, int B, int N) {
 }
 
 hipError_t launch_dense_offsets(int *offsets, int B, int N, hipStream_t s) {
-  hipLaunchKernelGGL(dense_offsets_kernel, dim3(1), dim3(256), 0, s, offsets, B, N);
+  rc_launch(dense_offsets_kernel, dim3(1), dim3(256), 0, s, offsets, B, N);
   return hipGetLastError();
 }
 
@@ -75,7 +76,7 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs a) {
 
 template <typename T> hipError_t launch_embed(const EmbedArgs &a, int R, hipStream_t s) {
   if (R <= 0) return hipSuccess;
-  hipLaunchKernelGGL(embed_kernel<T>, dim3(R), dim3(256), 0, s, a);
+  rc_launch(embed_kernel<T>, dim3(R), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 template hipError_t launch_embed<bf16>(const EmbedArgs &, int, hipStream_t);
@@ -97,25 +98,30 @@ template <> __device__ __forceinline__ void store4<bf16>(bf16 *p, float a, float
 template <typename T>
 __global__ __launch_bounds__(256) void ln_mod_kernel(const float *X, int R, int C, const float *table,
                                                      const float *t0, int shift_row, float eps, T *out) {
-  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (r >= R) return;
-  constexpr int MAXV = 6;  // C <= 64*4*MAXV
+  __shared__ float red[4];
+  const int r = blockIdx.x, t = threadIdx.x;  // one 256-thread workgroup per row
+  constexpr int MAXV = 2;                      // C <= 4 * 256 * MAXV
   const int C4 = C >> 2;
   const f32x4 *x = (const f32x4 *)(X + (size_t)r * C);
-  f32x4 v[MAXV];
+  const f32x4 *sh = (const f32x4 *)(table + (size_t)shift_row * C), *sc = (const f32x4 *)(table + (size_t)(shift_row + 1) * C);
+  const f32x4 *tsh = (const f32x4 *)(t0 + (size_t)shift_row * C), *tsc = (const f32x4 *)(t0 + (size_t)(shift_row + 1) * C);
+  // the row and its modulation rows are loaded together (one memory round trip)
+  f32x4 v[MAXV], shift[MAXV], scale[MAXV];
   float s = 0.0f;
 #pragma unroll
   for (int i = 0; i < MAXV; ++i) {
-    const int n = lane + i * 64;
-    v[i] = n < C4 ? x[n] : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    const int n = t + i * 256;
+    const f32x4 z = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    v[i] = n < C4 ? x[n] : z;
+    shift[i] = n < C4 ? sh[n] + tsh[n] : z;
+    scale[i] = n < C4 ? sc[n] + tsc[n] : z;
     s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
   }
-  const float mean = wave_sum(s) / C;
+  const float mean = block4_sum(s, red) / C;
   float q = 0.0f;
 #pragma unroll
   for (int i = 0; i < MAXV; ++i) {
-    const int n = lane + i * 64;
+    const int n = t + i * 256;
     if (n < C4)
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
@@ -123,18 +129,15 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const float *X, int R, int 
         q += d * d;
       }
   }
-  const float rstd = rsqrtf(wave_sum(q) / C + eps);
-  const f32x4 *sh = (const f32x4 *)(table + (size_t)shift_row * C), *sc = (const f32x4 *)(table + (size_t)(shift_row + 1) * C);
-  const f32x4 *tsh = (const f32x4 *)(t0 + (size_t)shift_row * C), *tsc = (const f32x4 *)(t0 + (size_t)(shift_row + 1) * C);
+  const float rstd = rsqrtf(block4_sum(q, red) / C + eps);
   T *o = out + (size_t)r * C;
 #pragma unroll
   for (int i = 0; i < MAXV; ++i) {
-    const int n = lane + i * 64;
+    const int n = t + i * 256;
     if (n < C4) {
-      const f32x4 a = sh[n], b = sc[n], ta = tsh[n], tb = tsc[n];
       float y[4];
 #pragma unroll
-      for (int k = 0; k < 4; ++k) y[k] = (v[i][k] - mean) * rstd * (1.0f + b[k] + tb[k]) + a[k] + ta[k];
+      for (int k = 0; k < 4; ++k) y[k] = (v[i][k] - mean) * rstd * (1.0f + scale[i][k]) + shift[i][k];
       store4<T>(o + 4 * n, y[0], y[1], y[2], y[3]);
     }
   }
@@ -144,8 +147,8 @@ template <typename T>
 hipError_t launch_ln_mod(const float *X, int R, int C, const float *table, const float *t0, int shift_row,
                          float eps, void *out, hipStream_t s) {
   if (R <= 0) return hipSuccess;
-  if (C > 64 * 4 * 6 || C % 4) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(ln_mod_kernel<T>, dim3((R + 3) / 4), dim3(256), 0, s, X, R, C, table, t0, shift_row, eps,
+  if (C > 4 * 256 * 2 || C % 4) return hipErrorInvalidValue;
+  rc_launch(ln_mod_kernel<T>, dim3(R), dim3(256), 0, s, X, R, C, table, t0, shift_row, eps,
                      (T *)out);
   return hipGetLastError();
 }
@@ -163,7 +166,7 @@ __global__ void timestep_features_kernel(float t, float *e) {
 }
 
 hipError_t launch_timestep_features(float t, float *e, hipStream_t s) {
-  hipLaunchKernelGGL(timestep_features_kernel, dim3(1), dim3(128), 0, s, t, e);
+  rc_launch(timestep_features_kernel, dim3(1), dim3(128), 0, s, t, e);
   return hipGetLastError();
 }
 
@@ -191,7 +194,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(const T *W, const float *bias
 template <typename T>
 hipError_t launch_gemv(const void *W, const float *bias, const float *x, int N, int K, int silu_in, int silu_out,
                        float *y, hipStream_t s) {
-  hipLaunchKernelGGL(gemv_kernel<T>, dim3((N + 3) / 4), dim3(256), 0, s, (const T *)W, bias, x, N, K, silu_in,
+  rc_launch(gemv_kernel<T>, dim3((N + 3) / 4), dim3(256), 0, s, (const T *)W, bias, x, N, K, silu_in,
                      silu_out, y);
   return hipGetLastError();
 }
@@ -277,7 +280,7 @@ template <typename T> hipError_t launch_final_ddim(const FinalArgs &a, hipStream
   if (a.R <= 0) return hipSuccess;
   if (a.C > 64 * 24 || a.out_ch < 4) return hipErrorInvalidValue;
   const size_t lds = (size_t)16 * a.C * sizeof(T);
-  hipLaunchKernelGGL(final_ddim_kernel<T>, dim3((a.R + FIN_ROWS - 1) / FIN_ROWS), dim3(256), lds, s, a);
+  rc_launch(final_ddim_kernel<T>, dim3((a.R + FIN_ROWS - 1) / FIN_ROWS), dim3(256), lds, s, a);
   return hipGetLastError();
 }
 template hipError_t launch_final_ddim<bf16>(const FinalArgs &, hipStream_t);
@@ -296,7 +299,7 @@ hipError_t launch_copy_chains(float *dst, long long dst_stride, const float *src
                               hipStream_t s) {
   const long tot = (long)n * B;
   if (tot <= 0) return hipSuccess;
-  hipLaunchKernelGGL(copy_chains_kernel, dim3((tot + 255) / 256), dim3(256), 0, s, dst, dst_stride, src, src_stride,
+  rc_launch(copy_chains_kernel, dim3((tot + 255) / 256), dim3(256), 0, s, dst, dst_stride, src, src_stride,
                      n, B);
   return hipGetLastError();
 }
@@ -318,7 +321,7 @@ hipError_t launch_scatter_rows(const int *offsets, const int *idx, int B, const 
   if (R <= 0) return hipSuccess;
   const int vpr = row_bytes / 16;
   const long tot = (long)R * vpr;
-  hipLaunchKernelGGL(scatter_rows_kernel, dim3((tot + 255) / 256), dim3(256), 0, s, offsets, idx, B,
+  rc_launch(scatter_rows_kernel, dim3((tot + 255) / 256), dim3(256), 0, s, offsets, idx, B,
                      (const V16 *)src, R, vpr, (V16 *)hslot, chain_stride_bytes / 16);
   return hipGetLastError();
 }
@@ -332,7 +335,7 @@ __global__ void zero_kernel(V16 *p, long n) {
 hipError_t launch_zero(void *p, size_t bytes, hipStream_t s) {
   const long n = bytes / 16;
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(zero_kernel, dim3((n + 255) / 256), dim3(256), 0, s, (V16 *)p, n);
+  rc_launch(zero_kernel, dim3((n + 255) / 256), dim3(256), 0, s, (V16 *)p, n);
   return hipGetLastError();
 }
 

@@ -10,6 +10,7 @@
 // LDS (rows padded by 16 bytes) with the next K step's global loads issued
 // before the current step's MFMAs.
 #include "rc_common.h"
+#include "rc_launch.h"
 #include "rc_internal.h"
 
 namespace rc {
@@ -166,11 +167,11 @@ template <typename T, int BM, int BN>
 static hipError_t launch_tile(const GemmArgs &a, int epi, hipStream_t s) {
   dim3 grid(a.N / BN, (a.M + BM - 1) / BM);
   switch (epi) {
-    case EPI_STORE: hipLaunchKernelGGL((gemm_kernel<T, BM, BN, EPI_STORE>), grid, dim3(256), 0, s, a); break;
-    case EPI_GELU: hipLaunchKernelGGL((gemm_kernel<T, BM, BN, EPI_GELU>), grid, dim3(256), 0, s, a); break;
-    case EPI_RESID: hipLaunchKernelGGL((gemm_kernel<T, BM, BN, EPI_RESID>), grid, dim3(256), 0, s, a); break;
-    case EPI_QKV: hipLaunchKernelGGL((gemm_kernel<T, BM, BN, EPI_QKV>), grid, dim3(256), 0, s, a); break;
-    case EPI_TEXTKV: hipLaunchKernelGGL((gemm_kernel<T, BM, BN, EPI_TEXTKV>), grid, dim3(256), 0, s, a); break;
+    case EPI_STORE: rc_launch(gemm_kernel<T, BM, BN, EPI_STORE>, grid, dim3(256), 0, s, a); break;
+    case EPI_GELU: rc_launch(gemm_kernel<T, BM, BN, EPI_GELU>, grid, dim3(256), 0, s, a); break;
+    case EPI_RESID: rc_launch(gemm_kernel<T, BM, BN, EPI_RESID>, grid, dim3(256), 0, s, a); break;
+    case EPI_QKV: rc_launch(gemm_kernel<T, BM, BN, EPI_QKV>, grid, dim3(256), 0, s, a); break;
+    case EPI_TEXTKV: rc_launch(gemm_kernel<T, BM, BN, EPI_TEXTKV>, grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -16,6 +16,7 @@
 //   one column panel of W) land on the same XCD (workgroups are dealt to the
 //   eight XCDs round-robin) and share that XCD's L2.
 #include "rc_common.h"
+#include "rc_launch.h"
 #include "rc_internal.h"
 
 #include <cmath>
@@ -84,6 +85,34 @@ __device__ __forceinline__ void st4(bf16 *p, const float *v) {
   *(bf16x4 *)p = o;
 }
 
+// X[m][n..n+3] += gate * v, with the E copies of the updated values; the
+// updated values are returned in v.
+__device__ __forceinline__ void resid4(const GemmArgs &g, int m, int n, float *v) {
+  f32x4 gt = f32x4{1.0f, 1.0f, 1.0f, 1.0f};
+  if (g.gate) {
+    gt = *(const f32x4 *)(g.gate + n);
+    if (g.gate2) {
+      const f32x4 g2 = *(const f32x4 *)(g.gate2 + n);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) gt[q] += g2[q];
+    }
+  }
+  f32x4 *xp = (f32x4 *)(g.X + (size_t)m * g.ldx + n);
+  f32x4 x = *xp;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    x[q] += gt[q] * v[q];
+    v[q] = x[q];
+  }
+  *xp = x;
+  if (g.xt) st4((bf16 *)g.xt + (size_t)m * g.ldx + n, v);
+  if (g.hrows) st4((bf16 *)g.hrows + (size_t)m * g.N + n, v);
+  if (g.hslot) {
+    const int pk = g.rows[m];
+    st4((bf16 *)g.hslot + row_chain(pk) * g.chain_stride + (size_t)row_token(pk) * g.hidden + n, v);
+  }
+}
+
 // Four consecutive output columns n..n+3 of row m (n % 4 == 0; never the
 // transposed-V part, whose columns are handled one by one).
 template <int EPI>
@@ -96,30 +125,7 @@ __device__ __forceinline__ void epi4(const GemmArgs &g, int m, int n, float *v, 
     for (int q = 0; q < 4; ++q) w[q] = gelu_tanh(v[q]);
     st4((bf16 *)g.out + (size_t)m * g.ldo + n, w);
   } else if (EPI == EPI_RESID) {
-    f32x4 gt = f32x4{1.0f, 1.0f, 1.0f, 1.0f};
-    if (g.gate) {
-      gt = *(const f32x4 *)(g.gate + n);
-      if (g.gate2) {
-        const f32x4 g2 = *(const f32x4 *)(g.gate2 + n);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) gt[q] += g2[q];
-      }
-    }
-    f32x4 *xp = (f32x4 *)(g.X + (size_t)m * g.ldx + n);
-    f32x4 x = *xp;
-    float xs[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      x[q] += gt[q] * v[q];
-      xs[q] = x[q];
-    }
-    *xp = x;
-    if (g.xt) st4((bf16 *)g.xt + (size_t)m * g.ldx + n, xs);
-    if (g.hrows) st4((bf16 *)g.hrows + (size_t)m * g.N + n, xs);
-    if (g.hslot) {
-      const int pk = g.rows[m];
-      st4((bf16 *)g.hslot + row_chain(pk) * g.chain_stride + (size_t)row_token(pk) * g.hidden + n, xs);
-    }
+    resid4(g, m, n, v);
   } else if (EPI == EPI_QKV) {
     if (part == 0) {
       st4((bf16 *)g.out + (size_t)m * g.ldo + n, v);
@@ -317,16 +323,17 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
       epi4<EPI>(g, m, n, v, tile_part);
     }
   } else {
-    for (int idx = tid; idx < BM * BN / 4; idx += NT) {
-      const int col = idx / (BM / 4), r4 = (idx % (BM / 4)) * 4;
+    // a wave walks one column, lanes on consecutive rows: each store covers
+    // consecutive tokens of one transposed-V row
+    static_assert(NT % BM == 0, "a pass must cover whole columns");
+    for (int idx = tid; idx < BM * BN; idx += NT) {
+      const int col = idx / BM, row = idx - col * BM;
+      const int m = m0 + row;
+      if (m >= g.M) continue;
       const int n = n0 + col;
       const float bn = g.bias ? g.bias[n] : 0.0f;
       const int c = n - tile_part * g.hidden, hh = c / kHeadDim, dd = c - hh * kHeadDim;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int m = m0 + r4 + q;
-        if (m < g.M) epi_store<EPI>(g, m, n, tile_at(r4 + q, col) + bn, 1.0f, tile_part, hh, dd);
-      }
+      epi_store<EPI>(g, m, n, tile_at(row, col) + bn, 1.0f, tile_part, hh, dd);
     }
   }
 }
@@ -346,12 +353,91 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(GemmArgs g, const fl
   epi_store<EPI>(g, m, n, v + bn, gate, part, hh, dd);
 }
 
+// Split reduction of a residual GEMM fused with the next block's LayerNorm:
+// one 256-thread workgroup per row sums the splits in order, adds bias,
+// applies gate and residual (with the E copies), then normalises the
+// finished row and writes the modulated E row for the next GEMM.
+template <int S>
+__global__ __launch_bounds__(256) void splitk_finish_ln_kernel(GemmArgs g, const float *partial, LnNext ln) {
+  __shared__ float red[4];
+  const int m = blockIdx.x, t = threadIdx.x;
+  constexpr int MAXV = 2;  // N <= 4 * 256 * MAXV
+  const int N4 = g.N >> 2;
+  const float *sh = ln.sst + (size_t)ln.shift_row * g.N, *sc = sh + g.N;
+  const float *tsh = ln.t0 + (size_t)ln.shift_row * g.N, *tsc = tsh + g.N;
+  // every load first (partials, bias, gate, residual, modulation), then the
+  // stores: the compiler may not move a load above a store to X
+  f32x4 p[MAXV], xo[MAXV], gt[MAXV], shift[MAXV], scale[MAXV];
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    const int n4 = t + 256 * i;
+    p[i] = xo[i] = shift[i] = scale[i] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    gt[i] = f32x4{1.0f, 1.0f, 1.0f, 1.0f};
+    if (n4 < N4) {
+      const int n = 4 * n4;
+      shift[i] = *(const f32x4 *)(sh + n) + *(const f32x4 *)(tsh + n);
+      scale[i] = *(const f32x4 *)(sc + n) + *(const f32x4 *)(tsc + n);
+#pragma unroll
+      for (int sp = 0; sp < S; ++sp) p[i] += *(const f32x4 *)(partial + ((size_t)sp * g.M + m) * g.N + n);
+      if (g.bias) p[i] += *(const f32x4 *)(g.bias + n);
+      if (g.gate) {
+        gt[i] = *(const f32x4 *)(g.gate + n);
+        if (g.gate2) gt[i] += *(const f32x4 *)(g.gate2 + n);
+      }
+      xo[i] = *(const f32x4 *)(g.X + (size_t)m * g.ldx + n);
+    }
+  }
+  float x[MAXV][4];
+  float sum = 0.0f;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    const int n4 = t + 256 * i;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) x[i][q] = xo[i][q] + gt[i][q] * p[i][q];
+    if (n4 < N4) {
+      const int n = 4 * n4;
+      *(f32x4 *)(g.X + (size_t)m * g.ldx + n) = f32x4{x[i][0], x[i][1], x[i][2], x[i][3]};
+      if (g.xt) st4((bf16 *)g.xt + (size_t)m * g.ldx + n, x[i]);
+      if (g.hrows) st4((bf16 *)g.hrows + (size_t)m * g.N + n, x[i]);
+      if (g.hslot) {
+        const int pk = g.rows[m];
+        st4((bf16 *)g.hslot + row_chain(pk) * g.chain_stride + (size_t)row_token(pk) * g.hidden + n, x[i]);
+      }
+      sum += (x[i][0] + x[i][1]) + (x[i][2] + x[i][3]);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) x[i][q] = 0.0f;
+    }
+  }
+  const float mean = block4_sum(sum, red) / g.N;
+  float sq = 0.0f;
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i)
+    if (t + 256 * i < N4)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float d = x[i][q] - mean;
+        sq += d * d;
+      }
+  const float rstd = rsqrtf(block4_sum(sq, red) / g.N + ln.eps);
+#pragma unroll
+  for (int i = 0; i < MAXV; ++i) {
+    const int n4 = t + 256 * i;
+    if (n4 < N4) {
+      float y[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) y[q] = (x[i][q] - mean) * rstd * (1.0f + scale[i][q]) + shift[i][q];
+      st4((bf16 *)ln.out + (size_t)m * g.N + 4 * n4, y);
+    }
+  }
+}
+
 template <int BM, int BN, int STAGES, int KG, int WGM, int WGN, bool SPLIT>
 static void launch_g2(const GemmArgs &a, int epi, int splits, float *partial, hipStream_t s) {
   dim3 grid(a.N / BN, (a.M + BM - 1) / BM, splits);
   const int kps = a.K / splits;
 #define RC_G2(E)                                                                                       \
-  hipLaunchKernelGGL((gemm2_kernel<BM, BN, STAGES, KG, WGM, WGN, E, SPLIT>), grid, dim3(64 * WGM * WGN * KG), 0, s, \
+  rc_launch(gemm2_kernel<BM, BN, STAGES, KG, WGM, WGN, E, SPLIT>, grid, dim3(64 * WGM * WGN * KG), 0, s, \
                      a, partial, kps)
   switch (epi) {
     case EPI_STORE: RC_G2(EPI_STORE); break;
@@ -366,7 +452,7 @@ static void launch_g2(const GemmArgs &a, int epi, int splits, float *partial, hi
 static void launch_reduce(const GemmArgs &a, int epi, int splits, const float *partial, hipStream_t s) {
   const long n = (long)a.M * a.N;
   dim3 grid((n + 255) / 256);
-#define RC_RD(E) hipLaunchKernelGGL(splitk_reduce_kernel<E>, grid, dim3(256), 0, s, a, partial, splits)
+#define RC_RD(E) rc_launch(splitk_reduce_kernel<E>, grid, dim3(256), 0, s, a, partial, splits)
   switch (epi) {
     case EPI_STORE: RC_RD(EPI_STORE); break;
     case EPI_GELU: RC_RD(EPI_GELU); break;
@@ -392,7 +478,9 @@ GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats) {
   return p;
 }
 
-hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &pl, float *partial, hipStream_t s) {
+hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &pl, float *partial, hipStream_t s,
+                        const LnNext *ln, bool *ln_done) {
+  if (ln_done) *ln_done = false;
   if (a.M <= 0) return hipSuccess;
   if (pl.bm != 64 || pl.bn != 128 || a.N % 128 || a.K % (G2_BK * pl.splits * pl.kg)) return hipErrorInvalidValue;
   const bool split = pl.splits > 1;
@@ -410,7 +498,16 @@ hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &pl, float *p
 #undef RC_G2_KG
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !split) return e;
-  launch_reduce(a, epi, pl.splits, partial, s);
+  if (ln && epi == EPI_RESID && a.N % 4 == 0 && a.N <= 4 * 256 * 2 && pl.splits <= 4) {
+    const dim3 grid(a.M), block(256);
+    const float *pp = partial;
+    if (pl.splits == 2) rc_launch(splitk_finish_ln_kernel<2>, grid, block, 0, s, a, pp, *ln);
+    else if (pl.splits == 3) rc_launch(splitk_finish_ln_kernel<3>, grid, block, 0, s, a, pp, *ln);
+    else rc_launch(splitk_finish_ln_kernel<4>, grid, block, 0, s, a, pp, *ln);
+    if (ln_done) *ln_done = true;
+  } else {
+    launch_reduce(a, epi, pl.splits, partial, s);
+  }
   return hipGetLastError();
 }
 

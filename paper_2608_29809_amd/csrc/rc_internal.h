@@ -73,7 +73,21 @@ struct GemmPlan {
   int waves;               // waves per K group: 4 (32x64 each), 2 (64x64) or 1 (64x128)
 };
 GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats);
-hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &plan, float *partial, hipStream_t s);
+// LayerNorm + modulation of the next block applied to the rows a residual
+// GEMM has just completed: out = E(LN(X) * (1 + scale) + shift) with shift and
+// scale = rows shift_row and shift_row+1 of sst + t0.
+struct LnNext {
+  const float *sst;
+  const float *t0;
+  int shift_row;
+  float eps;
+  void *out;  // [M][N] E
+};
+// With `ln` non-null and a split plan, the split reduction of an EPI_RESID
+// GEMM also applies `ln` (one pass over each finished row); *ln_done tells
+// the caller whether it did.
+hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &plan, float *partial, hipStream_t s,
+                        const LnNext *ln = nullptr, bool *ln_done = nullptr);
 template <typename T> hipError_t launch_attention(const AttnArgs &a, int n_chains, int max_rows,
                                                   bool emit_maps, hipStream_t s);
 // bf16 attention with direct-to-LDS tiles and uneven key splits (rc_attn2.hip).

@@ -3,6 +3,7 @@
 // from each map's range, union over delta tokens, grid dilation, and the
 // stable compaction of the resulting mask into per-chain token lists.
 #include "rc_common.h"
+#include "rc_launch.h"
 #include "rc_elem.h"
 
 namespace rc {
@@ -73,7 +74,7 @@ hipError_t launch_maps_from_logits(const uint16_t *logits, int n_layers, int hea
   dim3 grid((tokens + LG_ROWS - 1) / LG_ROWS, n_layers);
   const int ld = ((text_len / 8) & 1) ? text_len : text_len + 8;
   const size_t lds = (size_t)LG_ROWS * ld * sizeof(uint16_t);
-  hipLaunchKernelGGL(maps_from_logits_kernel, grid, dim3(256), lds, s, logits, heads, tokens, text_len, dl, partial);
+  rc_launch(maps_from_logits_kernel, grid, dim3(256), lds, s, logits, heads, tokens, text_len, dl, partial);
   return hipGetLastError();
 }
 
@@ -88,7 +89,7 @@ __global__ void sum_partials_kernel(const float *partial, int n_parts, int n, fl
 
 hipError_t launch_sum_partials(const float *partial, int n_parts, int n, float *out, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(sum_partials_kernel, dim3((n + 255) / 256), dim3(256), 0, s, partial, n_parts, n, out);
+  rc_launch(sum_partials_kernel, dim3((n + 255) / 256), dim3(256), 0, s, partial, n_parts, n, out);
   return hipGetLastError();
 }
 
@@ -152,7 +153,7 @@ __global__ __launch_bounds__(1024) void localize_kernel(const float *maps, int g
 
 hipError_t launch_localize(const float *maps, int B, int gh, int gw, int n_delta, float threshold, int radius,
                            uint8_t *mask, hipStream_t s) {
-  hipLaunchKernelGGL(localize_kernel, dim3(B), dim3(1024), (size_t)gh * gw, s, maps, gh, gw, n_delta, threshold,
+  rc_launch(localize_kernel, dim3(B), dim3(1024), (size_t)gh * gw, s, maps, gh, gw, n_delta, threshold,
                      radius, mask);
   return hipGetLastError();
 }
@@ -191,7 +192,7 @@ __global__ __launch_bounds__(1024) void compact_kernel(const uint8_t *mask, int 
 }
 
 hipError_t launch_compact(const uint8_t *mask, int B, int N, int *idx, int *offsets, hipStream_t s) {
-  hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(1024), 0, s, mask, B, N, idx, offsets);
+  rc_launch(compact_kernel, dim3(1), dim3(1024), 0, s, mask, B, N, idx, offsets);
   return hipGetLastError();
 }
 

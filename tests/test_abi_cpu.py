@@ -194,3 +194,13 @@ def test_kernel_timing_classes(ctx):
     with pytest.raises(abi.RcError):
         abi.rc_get_kernel_timing(ctx, abi.RC_KC_COUNT, C.byref(ms), C.byref(n))
     abi.rc_set_kernel_timing(ctx, 0)
+
+
+def test_kernel_class_table_matches_header():
+    """The binding's kernel-class constants and names follow the header's enum."""
+    import re
+    hdr = open(os.path.join(ROOT, "include", "regioncache.h")).read()
+    vals = {k: int(v) for k, v in re.findall(r"(RC_KC_\w+)\s*=\s*(\d+)", hdr)}
+    assert vals["RC_KC_COUNT"] == abi.RC_KC_COUNT == len(abi.KERNEL_CLASSES)
+    for k, v in vals.items():
+        assert getattr(abi, k) == v, k
