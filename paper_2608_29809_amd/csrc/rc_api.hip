@@ -372,12 +372,13 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       a.offsets = offsets_dev; a.n_keys = N; a.n_valid = N; a.hidden = C; a.splits = splits;
       a.O = O; a.Opart = part; a.ML = ml; a.total_rows = R; a.scale_log2 = scale_log2;
       RC_TRY(timed(c, RC_KC_ATTN_SELF, s, [&] {
-        return sizeof(T) == 2 ? rc::launch_attention2(a, B, max_rb, false, s)
+        return sizeof(T) == 2 ? rc::launch_attention3(a, B, max_rb, s)
                               : rc::launch_attention<T>(a, B, max_rb, false, s);
       }));
       if (splits > 1)
         RC_TRY(timed(c, RC_KC_ATTN_COMBINE, s, [&] {
-          return rc::launch_attn_combine(part, ml, O, sizeof(T) == 2, R, H, splits, s);
+          return sizeof(T) == 2 ? rc::launch_attn_combine_norm(part, ml, O, R, H, splits, s)
+                                : rc::launch_attn_combine(part, ml, O, false, R, H, splits, s);
         }));
     }
     {  // out-projection + gate + residual; E copy of X for the cross query

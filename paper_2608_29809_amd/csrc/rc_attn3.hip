@@ -1,0 +1,328 @@
+// bf16 self-attention, third form: the score MFMAs of key tile t+1 are issued
+// before the softmax of tile t, so the matrix core works on S(t+1) while the
+// vector ALUs exponentiate S(t) within the same wave.
+//
+// Decomposition, operand layouts and numerics are those of attn2_kernel
+// (rc_attn2.hip): 128 queries of one (chain, head, key range) per workgroup,
+// 32 per wave; S^T = K Q^T with the permuted key rows; O^T = V^T P^T with the
+// swizzled V^T tile and the ones row that accumulates the softmax
+// denominator; exp2 online softmax with the lazy rescale; uneven key splits
+// and the deterministic combine.  Differences:
+//
+// * a three-tile ring: while tile t's values are read and tile t+1's keys are
+//   read, tile t+2 streams in; one barrier per tile;
+// * the loop carries the scores of the next tile in registers.
+#include "rc_common.h"
+#include "rc_launch.h"
+#include "rc_internal.h"
+
+#include <type_traits>
+
+namespace rc {
+
+constexpr int A3_BQ = 128, A3_BK = 64, A3_STAGES = 3;
+
+__device__ __forceinline__ int key_perm3(int m) {
+  return ((m >> 4) & 1) * 16 + ((m >> 2) & 1) * 8 + ((m >> 3) & 1) * 4 + (m & 3);
+}
+__device__ __forceinline__ void lds_barrier3() { asm volatile("s_barrier" ::: "memory"); }
+__device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+__global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
+  constexpr int D = kHeadDim;
+  constexpr int KT_BYTES = A3_BK * D * 2;  // K tile [64][72]
+  constexpr int VT_BYTES = D * A3_BK * 2;  // V^T tile [72][64]
+  constexpr int STAGE = KT_BYTES + VT_BYTES;
+  constexpr int K_CH = KT_BYTES / 16;      // 576 16-byte chunks per operand tile
+  __shared__ __attribute__((aligned(1024))) char lds[A3_STAGES * STAGE + 128];
+  char *ones_row = lds + A3_STAGES * STAGE;
+  if (threadIdx.x < 8) *(V16 *)(ones_row + threadIdx.x * 16) = V16{{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u}};
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 5, r32 = lane & 31;
+  const int heads = a.hidden / D;
+  // XCD-aware order (query tiles of one (chain, head, key range) share an XCD)
+  const int G = gridDim.x, Y = gridDim.y, T = G * Y * gridDim.z;
+  const int p = blockIdx.x + G * (blockIdx.y + Y * blockIdx.z);
+  const int L = xcd_logical_id(p, T);
+  const int qt = L % G, hy = (L / G) % Y, b = L / (G * Y);
+  const int h = hy % heads, split = hy / heads;
+  const int r0 = a.offsets[b], r1 = a.offsets[b + 1];
+  const int q0 = r0 + qt * A3_BQ;
+  if (q0 >= r1) return;  // uniform across the workgroup
+  const int my_q = q0 + wave * 32 + r32;
+  const bool q_ok = my_q < r1;
+
+  const int n_tiles = a.n_keys / A3_BK;
+  const int t_beg = (int)((long)split * n_tiles / a.splits), t_end = (int)((long)(split + 1) * n_tiles / a.splits);
+  const bf16 *Kg = (const bf16 *)a.K + b * a.chain_stride + h * a.head_stride;
+  const bf16 *Vg = (const bf16 *)a.Vt + b * a.chain_stride + h * a.head_stride;
+
+  bf16x8 qf[5];
+  {
+    const bf16 *qrow = (const bf16 *)a.Q + (size_t)(q_ok ? my_q : q0) * a.hidden + h * D;
+#pragma unroll
+    for (int c = 0; c < 5; ++c) {
+      const int d0 = c * 16 + g * 8;
+      qf[c] = Mfma<bf16>::zero();
+      if (q_ok && d0 < D) qf[c] = *(const bf16x8 *)(qrow + d0);
+    }
+  }
+
+  auto issue = [&](int stage, int tile) {
+    char *ks = lds + stage * STAGE, *vs = ks + KT_BYTES;
+    const int key0 = tile * A3_BK;
+    const char *kt = (const char *)(Kg + (size_t)key0 * D);
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+      const int base = i * 256 + wave * 64;
+      if (base < K_CH)
+        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)(kt + (base + lane) * 16),
+                                         (__attribute__((address_space(3))) void *)(ks + base * 16), 16, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+      const int base = i * 256 + wave * 64;
+      if (base < K_CH) {
+        const int ch = base + lane, d = ch >> 3, lc = (ch & 7) ^ (d & 7);
+        const bf16 *src = Vg + (size_t)d * a.n_keys + key0 + lc * 8;
+        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
+                                         (__attribute__((address_space(3))) void *)(vs + base * 16), 16, 0, 0);
+      }
+    }
+  };
+  // S^T of one tile: lane group g, sub-tile st, accumulator e = c*8 + k  <->
+  // key st*32 + c*16 + g*8 + k
+  auto scores = [&](int stage, f32x16 *s) {
+    const char *ks = lds + stage * STAGE;
+    bf16x8 kf[2][5];
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      const char *krow = ks + (st * 32 + key_perm3(r32)) * (D * 2);
+#pragma unroll
+      for (int c = 0; c < 5; ++c) kf[st][c] = *(const bf16x8 *)(krow + (c * 16 + g * 8) * 2);
+      // d0 = 72 lies past the row (it reads the next row); zero it without a branch
+      kf[st][4] = (g == 0) ? kf[st][4] : Mfma<bf16>::zero();
+    }
+#pragma unroll
+    for (int c = 0; c < 5; ++c)
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+        s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st][c], qf[c], c == 0 ? f32x16{} : s[st], 0, 0, 0);
+  };
+
+  f32x16 o[3];
+#pragma unroll
+  for (int t = 0; t < 3; ++t)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) o[t][e] = 0.0f;
+  float m_run = -INFINITY;
+  const float c2 = a.scale_log2;
+
+  // prologue: tiles t_beg and t_beg+1 in flight, scores of t_beg
+  issue(0, t_beg);
+  if (t_beg + 1 < t_end) issue(1, t_beg + 1);
+  if (t_beg + 1 < t_end) {
+    if (wave == 0) asm volatile("s_waitcnt vmcnt(6)" ::: "memory");  // wave 0 issues 6 loads per tile, others 4
+    else asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+  } else {
+    wait_vm_all();
+  }
+  lds_barrier3();
+  f32x16 s_cur[2];
+  scores(0, s_cur);
+
+  // One key tile: wait for tile+1 and recycle the slot of tile-1, update the
+  // running maximum, then (one basic block) the score MFMAs of tile+1
+  // interleaved with the exponentials of tile, then the PV MFMAs of tile.
+  auto step = [&](int tile, auto has_next_c) {
+    constexpr bool HAS_NEXT = decltype(has_next_c)::value;
+    const int stage = (tile - t_beg) % A3_STAGES;
+    // tile+1 has landed (the only loads in flight) and every wave is done with
+    // tile-1, whose slot takes tile+2
+    wait_vm_all();
+    lds_barrier3();
+    if (tile + 2 < t_end) issue((tile - t_beg + 2) % A3_STAGES, tile + 2);
+    bf16x8 kf[2][5];
+    if (HAS_NEXT) {
+      const char *ks = lds + ((tile - t_beg + 1) % A3_STAGES) * STAGE;
+#pragma unroll
+      for (int st = 0; st < 2; ++st) {
+        const char *krow = ks + (st * 32 + key_perm3(r32)) * (D * 2);
+#pragma unroll
+        for (int c = 0; c < 5; ++c) kf[st][c] = *(const bf16x8 *)(krow + (c * 16 + g * 8) * 2);
+        kf[st][4] = (g == 0) ? kf[st][4] : Mfma<bf16>::zero();
+      }
+    }
+
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, s_cur[st][e]);
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    // lazy rescale: the reference maximum moves only when some query of the
+    // wave gained more than 2^8 over it
+    const float m_new = fmaxf(m_run, tmax);
+    if (__any((m_new - m_run) * c2 > 8.0f)) {
+      const float alpha = (m_run == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m_run - m_new) * c2);
+#pragma unroll
+      for (int t = 0; t < 3; ++t)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[t][e] *= alpha;
+      m_run = m_new;
+    }
+    const float mc = (m_run == -INFINITY) ? 0.0f : m_run * c2;
+
+    f32x16 s_next[2];
+    if (HAS_NEXT) {
+#pragma unroll
+      for (int c = 0; c < 5; ++c)
+#pragma unroll
+        for (int st = 0; st < 2; ++st)
+          s_next[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st][c], qf[c], c == 0 ? f32x16{} : s_next[st], 0, 0, 0);
+    }
+    bf16x8 pf[2][2];
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+          pf[st][c][k] = (bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[st][c * 8 + k], c2, -mc));
+    if (HAS_NEXT) {
+      // one score MFMA, then a run of softmax VALU work, ten times
+#pragma unroll
+      for (int i = 0; i < 10; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);  // VALU
+      }
+    }
+
+    const char *vs = lds + stage * STAGE + KT_BYTES;
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const int lc = st * 4 + c * 2 + g;
+#pragma unroll
+        for (int t = 0; t < 3; ++t) {
+          // rows d >= 72 feed output rows that are never stored: clamped reads
+          const int d = min(t * 32 + r32, D - 1);
+          const char *va = vs + d * 128 + ((lc ^ (d & 7)) << 4);
+          if (t == 2 && r32 == 8) va = ones_row + (lc << 4);
+          const bf16x8 vf = *(const bf16x8 *)va;
+          o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[st][c], o[t], 0, 0, 0);
+        }
+      }
+    if (HAS_NEXT) {
+      s_cur[0] = s_next[0];
+      s_cur[1] = s_next[1];
+    }
+  };
+  for (int tile = t_beg; tile + 1 < t_end; ++tile) step(tile, std::true_type{});
+  step(t_end - 1, std::false_type{});
+
+  const float l_tot = __shfl(o[2][4], r32, 64);  // output row 72: the denominator
+  if (!q_ok) return;
+  if (a.splits == 1) {
+    const float inv = 1.0f / l_tot;
+    bf16 *orow = (bf16 *)a.O + (size_t)my_q * a.hidden + h * D;
+#pragma unroll
+    for (int t = 0; t < 3; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int d = t * 32 + i * 8 + g * 4;
+        if (d < D) {
+          bf16x4 v;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v[j] = (bf16)(o[t][i * 4 + j] * inv);
+          *(bf16x4 *)(orow + d) = v;
+        }
+      }
+  } else {
+    // a split stores its own normalised output (a convex combination of
+    // value rows, so bf16 keeps its relative precision) with its log2-domain
+    // maximum and denominator; the combine re-weights the splits
+    const float inv = 1.0f / l_tot;
+    bf16 *orow = (bf16 *)a.Opart + ((size_t)split * a.total_rows + my_q) * a.hidden + h * D;
+#pragma unroll
+    for (int t = 0; t < 3; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int d = t * 32 + i * 8 + g * 4;
+        if (d < D) {
+          bf16x4 v;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v[j] = (bf16)(o[t][i * 4 + j] * inv);
+          *(bf16x4 *)(orow + d) = v;
+        }
+      }
+    if (g == 0) {
+      float *ml = a.ML + (((size_t)split * a.total_rows + my_q) * heads + h) * 2;
+      ml[0] = m_run * c2;
+      ml[1] = l_tot;
+    }
+  }
+}
+
+// Combine of normalised bf16 split outputs: O = sum_s w_s O_s / sum_s w_s with
+// w_s = 2^(m_s - max m) l_s, in split order.  One thread per (row, head,
+// 8 dims); all loads are issued before use.
+__global__ __launch_bounds__(256) void attn_combine_norm_kernel(const bf16 *Opart, const float *ML, bf16 *O, int R,
+                                                                int heads, int splits) {
+  constexpr int G = kHeadDim / 8;
+  const int C = heads * kHeadDim;
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long)R * heads * G) return;
+  const int r = idx / (heads * G);
+  const int rem = idx - (long)r * heads * G;
+  const int h = rem / G, d = (rem - h * G) * 8;
+  constexpr int SMAX = 16;
+  float2 ml[SMAX];
+  bf16x8 p[SMAX];
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s)
+    if (s < splits) {
+      ml[s] = *(const float2 *)(ML + (((size_t)s * R + r) * heads + h) * 2);
+      p[s] = *(const bf16x8 *)(Opart + ((size_t)s * R + r) * C + h * kHeadDim + d);
+    }
+  float M = -INFINITY;
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s)
+    if (s < splits) M = fmaxf(M, ml[s].x);
+  float num[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f}, den = 0.0f;
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s)
+    if (s < splits) {
+      const float w = exp2f(ml[s].x - M) * ml[s].y;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) num[k] += w * (float)p[s][k];
+      den += w;
+    }
+  const float inv = 1.0f / den;
+  bf16x8 v;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) v[k] = (bf16)(num[k] * inv);
+  *(bf16x8 *)(O + (size_t)r * C + h * kHeadDim + d) = v;
+}
+
+hipError_t launch_attn_combine_norm(const void *Opart, const float *ML, void *O, int R, int heads, int splits,
+                                    hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  if (splits < 1 || splits > 16) return hipErrorInvalidValue;
+  const long n = (long)R * heads * (kHeadDim / 8);
+  rc_launch(attn_combine_norm_kernel, dim3((n + 255) / 256), dim3(256), 0, s, (const bf16 *)Opart, ML, (bf16 *)O, R,
+            heads, splits);
+  return hipGetLastError();
+}
+
+hipError_t launch_attention3(const AttnArgs &a, int n_chains, int max_rows, hipStream_t s) {
+  if (max_rows <= 0) return hipSuccess;
+  if (a.n_keys % A3_BK != 0 || a.splits < 1 || a.splits > a.n_keys / A3_BK) return hipErrorInvalidValue;
+  dim3 grid((max_rows + A3_BQ - 1) / A3_BQ, (a.hidden / kHeadDim) * a.splits, n_chains);
+  rc_launch(attn3_kernel, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace rc

@@ -463,18 +463,41 @@ static void launch_reduce(const GemmArgs &a, int epi, int splits, const float *p
 #undef RC_RD
 }
 
-// Choice of tile, K groups and split count for a shape (measured on the
-// step's shapes with cold weights: 723 and 4096 rows, N in {1152, 3456,
-// 4608}, K in {1152, 4608}).  64x128 tiles throughout.  When the grid has few
-// tiles (the N = 1152 GEMMs at a few hundred rows) a workgroup runs two K
-// groups of four waves, which doubles the waves per CU without global
-// partials; split-K over the grid only pays for K = 4608 with few tiles.
+// Choice of tile, K groups and split count for a shape, from sweeps on the
+// step's shapes with cold weights (412, 723 and 4096 rows; N in {1152, 3456,
+// 4608}; K in {1152, 4608}).  A K step costs roughly the same time whatever
+// the tile, so a workgroup's time is set by its K steps: when the grid is
+// small the rows are cut into 32-row tiles and K over two groups of waves in
+// one workgroup (each CU runs one such workgroup), as long as the grid still
+// fits the 256 CUs in one wave of workgroups; large grids keep 64x128 tiles
+// with two workgroups per CU.  Split-K over the grid only pays for K = 4608
+// at few tiles.
 GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats) {
-  GemmPlan p{64, 128, 1, 1, 4};
-  const long tiles = (long)((M + 63) / 64) * (N / 128);
+  GemmPlan p{64, 128, 1, 1, 2};
   const int nk = K / G2_BK;
-  if (tiles < 160 && nk % 2 == 0) p.kg = 2;
-  if (K >= 2048 && tiles < 384 && nk % (2 * p.kg) == 0 && (size_t)2 * M * N <= partial_cap_floats) p.splits = 2;
+  const long t64 = (long)((M + 63) / 64) * (N / 128), t32 = (long)((M + 31) / 32) * (N / 128);
+  if (K >= 2048) {
+    if (t64 < 384 && nk % 4 == 0 && (size_t)2 * M * N <= partial_cap_floats) {
+      p.splits = 2;
+      p.kg = 2;
+      p.stages = 3;
+      if (t32 * 2 <= 256) p.bm = 32;
+    } else if (t64 < 160 && nk % 2 == 0) {
+      p.kg = 2;
+      p.stages = 3;
+    }
+    return p;
+  }
+  if (nk % 2 == 0) {
+    if (t32 <= 256) {
+      p.bm = 32;
+      p.kg = 2;
+      p.stages = 3;
+    } else if (t64 <= 256) {
+      p.kg = 2;
+      p.stages = 3;
+    }
+  }
   return p;
 }
 
@@ -482,20 +505,24 @@ hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &pl, float *p
                         const LnNext *ln, bool *ln_done) {
   if (ln_done) *ln_done = false;
   if (a.M <= 0) return hipSuccess;
-  if (pl.bm != 64 || pl.bn != 128 || a.N % 128 || a.K % (G2_BK * pl.splits * pl.kg)) return hipErrorInvalidValue;
+  if (pl.bn != 128 || a.N % 128 || a.K % (G2_BK * pl.splits * pl.kg)) return hipErrorInvalidValue;
   const bool split = pl.splits > 1;
-  // wave layouts: 4 = 2x2 waves of 32x64, 2 = 1x2 waves of 64x64, 1 = one wave of 64x128
-#define RC_G2_KG(KGV, STG, WM_, WN_)                                   \
-  if (split) launch_g2<64, 128, STG, KGV, WM_, WN_, true>(a, epi, pl.splits, partial, s); \
-  else launch_g2<64, 128, STG, KGV, WM_, WN_, false>(a, epi, 1, nullptr, s);
-  if (pl.waves == 4) {
-    if (pl.kg == 2) { RC_G2_KG(2, 3, 2, 2) } else { RC_G2_KG(1, 2, 2, 2) }
-  } else if (pl.waves == 2) {
-    if (pl.kg == 2) { RC_G2_KG(2, 3, 1, 2) } else { RC_G2_KG(1, 2, 1, 2) }
-  } else {
-    if (pl.kg == 2) { RC_G2_KG(2, 3, 1, 1) } else { RC_G2_KG(1, 2, 1, 1) }
+  // tile shapes: 64 rows = 2x2 waves of 32x64; 32 rows = 1x4 waves of 32x32
+#define RC_G2(BMV, KGV, STG, WM_, WN_)                                                       \
+  {                                                                                          \
+    if (split) launch_g2<BMV, 128, STG, KGV, WM_, WN_, true>(a, epi, pl.splits, partial, s); \
+    else launch_g2<BMV, 128, STG, KGV, WM_, WN_, false>(a, epi, 1, nullptr, s);              \
   }
-#undef RC_G2_KG
+  const int cfg = pl.bm * 100 + pl.kg * 10 + pl.stages;
+  switch (cfg) {
+    case 6412: RC_G2(64, 1, 2, 2, 2) break;
+    case 6423: RC_G2(64, 2, 3, 2, 2) break;
+    case 3213: RC_G2(32, 1, 3, 1, 4) break;
+    case 3223: RC_G2(32, 2, 3, 1, 4) break;
+    case 3232: RC_G2(32, 3, 2, 1, 4) break;
+    default: return hipErrorInvalidValue;
+  }
+#undef RC_G2
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !split) return e;
   if (ln && epi == EPI_RESID && a.N % 4 == 0 && a.N <= 4 * 256 * 2 && pl.splits <= 4) {

@@ -55,7 +55,7 @@ struct AttnArgs {
   int hidden;            // C = heads*72
   int splits;            // key-range splits (grid.y = heads*splits)
   void *O;               // [R][C] E output (splits == 1)
-  float *Opart;          // [splits][R][C] unnormalised partial outputs (splits > 1)
+  float *Opart;          // [splits][R][C] split outputs (splits > 1): fp32 unnormalised (fp32 path) or bf16 normalised (launch_attention3)
   float *ML;             // [splits][R][heads][2] running max (log2 domain) and sum
   int total_rows;        // R (stride of the partial arrays)
   // map emission (cross-attention)
@@ -69,8 +69,8 @@ template <typename T> hipError_t launch_gemm(const GemmArgs &a, int epi, hipStre
 
 // bf16 GEMM with direct-to-LDS staging and optional split-K (rc_gemm2.hip).
 struct GemmPlan {
-  int bm, bn, splits, kg;  // kg: K groups inside one workgroup
-  int waves;               // waves per K group: 4 (32x64 each), 2 (64x64) or 1 (64x128)
+  int bm, bn, splits, kg;  // kg: K groups inside one workgroup (4 waves each)
+  int stages;              // LDS ring depth per K group
 };
 GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats);
 // LayerNorm + modulation of the next block applied to the rows a residual
@@ -92,6 +92,13 @@ template <typename T> hipError_t launch_attention(const AttnArgs &a, int n_chain
                                                   bool emit_maps, hipStream_t s);
 // bf16 attention with direct-to-LDS tiles and uneven key splits (rc_attn2.hip).
 hipError_t launch_attention2(const AttnArgs &a, int n_chains, int max_rows, bool cross, hipStream_t s);
+// bf16 self-attention with the next tile's score MFMAs overlapping the
+// softmax (rc_attn3.hip); no map emission.
+hipError_t launch_attention3(const AttnArgs &a, int n_chains, int max_rows, hipStream_t s);
+// Split combine for launch_attention3: Opart holds normalised bf16 split
+// outputs [splits][R][C], ML the log2-domain maxima and denominators.
+hipError_t launch_attn_combine_norm(const void *Opart, const float *ML, void *O, int R, int heads, int splits,
+                                    hipStream_t s);
 hipError_t launch_attn_combine(const float *Opart, const float *ML, void *O, bool bf16_out, int R,
                                int heads, int splits, hipStream_t s);
 hipError_t launch_maps_reduce(const float *pmaps, const int *rows, float *maps, int R, int heads,
