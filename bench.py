@@ -386,8 +386,9 @@ def sweep_leg(model1, args):
 
 
 KERNEL_SOURCES = {  # sources whose text fixes a kernel class's code
-    "attn": ["rc_attn2.hip", "rc_common.h", "rc_internal.h"],
-    "gemm": ["rc_gemm2.hip", "rc_common.h", "rc_internal.h"],
+    "attn_self": ["rc_attn3.hip", "rc_common.h", "rc_internal.h", "rc_launch.h"],
+    "attn_cross": ["rc_attn2.hip", "rc_common.h", "rc_internal.h", "rc_launch.h"],
+    "gemm": ["rc_gemm2.hip", "rc_common.h", "rc_internal.h", "rc_launch.h"],
 }
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "hbm_traffic_reuse_step_1024px.md")
 
@@ -395,7 +396,7 @@ TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "hbm_traffic_reuse_step_1024px.
 def kernel_source_hash(cls):
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES["attn" if cls.startswith("attn") else "gemm"]:
+    for f in KERNEL_SOURCES.get(cls, KERNEL_SOURCES["gemm"]):
         h.update(open(os.path.join(ROOT, "paper_2608_29809_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 

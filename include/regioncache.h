@@ -194,7 +194,7 @@ rc_status rc_prepare_text(rc_ctx *ctx, const void *txt, int32_t batch, void *tex
 /* Inputs of one step.
  *   input   -- device; latent float32 [batch][c][2gh][2gw] (the x_t entering
  *              the step), or in token mode hidden tokens E [batch][N][C].
- *   t_vec   -- token mode only: device float32 [C] timestep vector; else NULL.
+ *   t_vec   -- token mode only: device float32 [C] timestep vector, 16-byte aligned; else NULL.
  *   timestep, timestep_next -- integer DDPM timesteps of this step and of the
  *              next one (-1 after the last step); ignored in token mode.
  *   text_kv -- from rc_prepare_text for the same batch.

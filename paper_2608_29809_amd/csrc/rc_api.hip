@@ -199,6 +199,7 @@ rc_status check_io(const rc_ctx *c, const rc_step_io *io) {
   }
   if (c->cfg.token_mode) {
     RC_CHECK(io->t_vec, RC_ERR_INVALID_ARG, "token mode needs t_vec");
+    RC_CHECK(aligned16(io->t_vec), RC_ERR_ALIGN, "io->t_vec not 16-byte aligned");
   } else {
     RC_CHECK(io->latent_out, RC_ERR_INVALID_ARG, "io->latent_out is null");
     RC_CHECK(io->timestep >= 0 && io->timestep < 1000, RC_ERR_INVALID_ARG, "timestep %d outside [0, 1000)",

@@ -71,27 +71,10 @@ __global__ __launch_bounds__(256, 2) void attn2_kernel(AttnArgs a) {
   const int L = xcd_logical_id(p, T);
   const int qt = L % G, hy = (L / G) % Y, b = L / (G * Y);
   const int h = hy % heads, split = hy / heads;
-  const int r0 = a.offsets[b], r1 = a.offsets[b + 1];
-  const int q0 = r0 + qt * A2_BQ;
-  if (q0 >= r1) return;  // uniform across the workgroup
-  const int my_q = q0 + wave * 32 + r32;
-  const bool q_ok = my_q < r1;
-
   const int n_tiles = a.n_keys / A2_BK;
   const int t_beg = (int)((long)split * n_tiles / a.splits), t_end = (int)((long)(split + 1) * n_tiles / a.splits);
   const bf16 *Kg = (const bf16 *)a.K + b * a.chain_stride + h * a.head_stride;
   const bf16 *Vg = (const bf16 *)a.Vt + b * a.chain_stride + h * a.head_stride;
-
-  bf16x8 qf[5];
-  {
-    const bf16 *qrow = (const bf16 *)a.Q + (size_t)(q_ok ? my_q : q0) * a.hidden + h * D;
-#pragma unroll
-    for (int c = 0; c < 5; ++c) {
-      const int d0 = c * 16 + g * 8;
-      qf[c] = Mfma<bf16>::zero();
-      if (q_ok && d0 < D) qf[c] = *(const bf16x8 *)(qrow + d0);
-    }
-  }
 
   auto issue = [&](int stage, int tile) {
     char *ks = lds + stage * STAGE, *vs = ks + KT_BYTES;
@@ -116,6 +99,32 @@ __global__ __launch_bounds__(256, 2) void attn2_kernel(AttnArgs a) {
     }
   };
 
+  // the first key tiles depend only on (chain, head, key range): they are in
+  // flight while the row offsets and the queries are fetched
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (t_beg + s < t_end) issue(s, t_beg + s);
+
+  const int r0 = a.offsets[b], r1 = a.offsets[b + 1];
+  const int q0 = r0 + qt * A2_BQ;
+  if (q0 >= r1) {  // uniform across the workgroup; no LDS write may land after exit
+    wait_vm0();
+    return;
+  }
+  const int my_q = q0 + wave * 32 + r32;
+  const bool q_ok = my_q < r1;
+
+  bf16x8 qf[5];
+  {
+    const bf16 *qrow = (const bf16 *)a.Q + (size_t)(q_ok ? my_q : q0) * a.hidden + h * D;
+#pragma unroll
+    for (int c = 0; c < 5; ++c) {
+      const int d0 = c * 16 + g * 8;
+      qf[c] = Mfma<bf16>::zero();
+      if (q_ok && d0 < D) qf[c] = *(const bf16x8 *)(qrow + d0);
+    }
+  }
+
   f32x16 o[3];
 #pragma unroll
   for (int t = 0; t < 3; ++t)
@@ -130,9 +139,6 @@ __global__ __launch_bounds__(256, 2) void attn2_kernel(AttnArgs a) {
   // ring of STAGES tiles: tiles t+1 .. t+STAGES-1 are in flight while tile t
   // is consumed.  Wave 0 issues 6 loads per tile (the 576-chunk K and V
   // tiles leave 64 chunks each over), the other waves 4.
-#pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
-    if (t_beg + s < t_end) issue(s, t_beg + s);
   for (int tile = t_beg; tile < t_end; ++tile) {
     const int stage = (tile - t_beg) % STAGES;
     if (tile + STAGES - 2 < t_end) {

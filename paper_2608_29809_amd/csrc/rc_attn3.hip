@@ -47,27 +47,10 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
   const int L = xcd_logical_id(p, T);
   const int qt = L % G, hy = (L / G) % Y, b = L / (G * Y);
   const int h = hy % heads, split = hy / heads;
-  const int r0 = a.offsets[b], r1 = a.offsets[b + 1];
-  const int q0 = r0 + qt * A3_BQ;
-  if (q0 >= r1) return;  // uniform across the workgroup
-  const int my_q = q0 + wave * 32 + r32;
-  const bool q_ok = my_q < r1;
-
   const int n_tiles = a.n_keys / A3_BK;
   const int t_beg = (int)((long)split * n_tiles / a.splits), t_end = (int)((long)(split + 1) * n_tiles / a.splits);
   const bf16 *Kg = (const bf16 *)a.K + b * a.chain_stride + h * a.head_stride;
   const bf16 *Vg = (const bf16 *)a.Vt + b * a.chain_stride + h * a.head_stride;
-
-  bf16x8 qf[5];
-  {
-    const bf16 *qrow = (const bf16 *)a.Q + (size_t)(q_ok ? my_q : q0) * a.hidden + h * D;
-#pragma unroll
-    for (int c = 0; c < 5; ++c) {
-      const int d0 = c * 16 + g * 8;
-      qf[c] = Mfma<bf16>::zero();
-      if (q_ok && d0 < D) qf[c] = *(const bf16x8 *)(qrow + d0);
-    }
-  }
 
   auto issue = [&](int stage, int tile) {
     char *ks = lds + stage * STAGE, *vs = ks + KT_BYTES;
@@ -91,6 +74,31 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
       }
     }
   };
+  // the first two key tiles depend only on (chain, head, key range): they
+  // are in flight while the row offsets and the queries are fetched
+  issue(0, t_beg);
+  if (t_beg + 1 < t_end) issue(1, t_beg + 1);
+
+  const int r0 = a.offsets[b], r1 = a.offsets[b + 1];
+  const int q0 = r0 + qt * A3_BQ;
+  if (q0 >= r1) {  // uniform across the workgroup; no LDS write may land after exit
+    wait_vm_all();
+    return;
+  }
+  const int my_q = q0 + wave * 32 + r32;
+  const bool q_ok = my_q < r1;
+
+  bf16x8 qf[5];
+  {
+    const bf16 *qrow = (const bf16 *)a.Q + (size_t)(q_ok ? my_q : q0) * a.hidden + h * D;
+#pragma unroll
+    for (int c = 0; c < 5; ++c) {
+      const int d0 = c * 16 + g * 8;
+      qf[c] = Mfma<bf16>::zero();
+      if (q_ok && d0 < D) qf[c] = *(const bf16x8 *)(qrow + d0);
+    }
+  }
+
   // S^T of one tile: lane group g, sub-tile st, accumulator e = c*8 + k  <->
   // key st*32 + c*16 + g*8 + k
   auto scores = [&](int stage, f32x16 *s) {
@@ -119,9 +127,8 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
   float m_run = -INFINITY;
   const float c2 = a.scale_log2;
 
-  // prologue: tiles t_beg and t_beg+1 in flight, scores of t_beg
-  issue(0, t_beg);
-  if (t_beg + 1 < t_end) issue(1, t_beg + 1);
+  // prologue: wait for tile t_beg (every load issued after its last one --
+  // tile t_beg+1, the queries -- may still be in flight), scores of t_beg
   if (t_beg + 1 < t_end) {
     if (wave == 0) asm volatile("s_waitcnt vmcnt(6)" ::: "memory");  // wave 0 issues 6 loads per tile, others 4
     else asm volatile("s_waitcnt vmcnt(4)" ::: "memory");

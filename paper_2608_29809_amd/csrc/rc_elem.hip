@@ -171,6 +171,24 @@ hipError_t launch_timestep_features(float t, float *e, hipStream_t s) {
 }
 
 // y[n] = act_out( W[n] . act_in(x) + b[n] ), one wave per output.
+// 8 consecutive inputs of one row as floats (16-byte loads).
+template <typename T> __device__ __forceinline__ void load8(const T *p, float *v);
+template <> __device__ __forceinline__ void load8<float>(const float *p, float *v) {
+  const f32x4 a = *(const f32x4 *)p, b = *(const f32x4 *)(p + 4);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    v[q] = a[q];
+    v[4 + q] = b[q];
+  }
+}
+template <> __device__ __forceinline__ void load8<bf16>(const bf16 *p, float *v) {
+  const bf16x8 a = *(const bf16x8 *)p;
+#pragma unroll
+  for (int q = 0; q < 8; ++q) v[q] = (float)a[q];
+}
+
+// y[n] = act(W[n] . act_in(x) + b[n]); one wave per output, each lane takes
+// 8 consecutive inputs per pass (K % 8 == 0, K <= 1536), every load first.
 template <typename T>
 __global__ __launch_bounds__(256) void gemv_kernel(const T *W, const float *bias, const float *x, int N, int K,
                                                    int silu_in, int silu_out, float *y) {
@@ -178,12 +196,24 @@ __global__ __launch_bounds__(256) void gemv_kernel(const T *W, const float *bias
   const int lane = threadIdx.x & 63;
   if (n >= N) return;
   const T *w = W + (size_t)n * K;
-  float acc = 0.0f;
-  for (int k = lane; k < K; k += 64) {
-    float xv = x[k];
-    if (silu_in) xv = silu(xv);
-    acc += to_f<T>(w[k]) * xv;
+  constexpr int MAXC = 3;
+  float wv[MAXC][8], xv[MAXC][8];
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    const int k0 = 8 * (lane + 64 * i);
+    if (k0 < K) {
+      load8<T>(w + k0, wv[i]);
+      load8<float>(x + k0, xv[i]);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) wv[i][q] = xv[i][q] = 0.0f;
+    }
   }
+  float acc = 0.0f;
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc += wv[i][q] * (silu_in ? silu(xv[i][q]) : xv[i][q]);
   acc = wave_sum(acc);
   if (lane == 0) {
     float v = acc + (bias ? bias[n] : 0.0f);
@@ -194,6 +224,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(const T *W, const float *bias
 template <typename T>
 hipError_t launch_gemv(const void *W, const float *bias, const float *x, int N, int K, int silu_in, int silu_out,
                        float *y, hipStream_t s) {
+  if (K % 8 || K > 64 * 8 * 3) return hipErrorInvalidValue;
   rc_launch(gemv_kernel<T>, dim3((N + 3) / 4), dim3(256), 0, s, (const T *)W, bias, x, N, K, silu_in,
                      silu_out, y);
   return hipGetLastError();
@@ -206,7 +237,7 @@ template hipError_t launch_gemv<float>(const void *, const float *, const float 
 // to the output latent and (if given) to the cached trajectory entry.  A
 // workgroup stages the 16 noise rows of W_f in LDS once and serves 8 rows
 // (two per wave); each output is a wave-wide dot product.
-constexpr int FIN_ROWS = 8;
+constexpr int FIN_ROWS = 4;  // one row per wave
 
 template <typename T>
 __global__ __launch_bounds__(256) void final_ddim_kernel(FinalArgs a) {
@@ -214,71 +245,95 @@ __global__ __launch_bounds__(256) void final_ddim_kernel(FinalArgs a) {
   T *wl = (T *)fin_lds;  // [16][C]: output o = pix*4 + c is W_f row pix*out_ch + c
   const int C = a.C, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const T *W = (const T *)a.fin_w;
-  for (int i = threadIdx.x; i < 16 * C; i += 256) {
-    const int o = i / C, n = i - o * C;
-    wl[i] = W[(size_t)((o >> 2) * a.out_ch + (o & 3)) * C + n];
+  {
+    constexpr int EPC = 16 / sizeof(T);  // elements per 16-byte chunk
+    const int cpr = C / EPC;
+    for (int i = threadIdx.x; i < 16 * cpr; i += 256) {
+      const int o = i / cpr, j = i - o * cpr;
+      *(V16 *)(wl + (size_t)o * C + j * EPC) = *(const V16 *)(W + (size_t)((o >> 2) * a.out_ch + (o & 3)) * C + j * EPC);
+    }
   }
   __syncthreads();
-  constexpr int MAXV = 24;
-  for (int rr = 0; rr < FIN_ROWS / 4; ++rr) {
-    const int r = blockIdx.x * FIN_ROWS + wave * (FIN_ROWS / 4) + rr;
-    if (r >= a.R) break;
-    const float *x = a.X + (size_t)r * C;
-    float v[MAXV];
-    float s = 0.0f;
+  const int r = blockIdx.x * FIN_ROWS + wave;
+  if (r >= a.R) return;
+  // lane chunk i holds inputs 8*(lane + 64 i) .. +8 (C % 8 == 0, C <= 1536)
+  constexpr int MAXC = 3;
+  const float *x = a.X + (size_t)r * C;
+  float v[MAXC][8], sh[MAXC][8], sc[MAXC][8];
+  float s = 0.0f;
 #pragma unroll
-    for (int i = 0; i < MAXV; ++i) {
-      const int n = lane + i * 64;
-      v[i] = n < C ? x[n] : 0.0f;
-      s += v[i];
-    }
-    const float mean = wave_sum(s) / C;
-    float q = 0.0f;
+  for (int i = 0; i < MAXC; ++i) {
+    const int k0 = 8 * (lane + 64 * i);
+    if (k0 < C) {
+      float t0[8];
+      load8<float>(x + k0, v[i]);
+      load8<float>(a.fin_sst + k0, sh[i]);
+      load8<float>(a.fin_sst + C + k0, sc[i]);
+      load8<float>(a.t_emb + k0, t0);
 #pragma unroll
-    for (int i = 0; i < MAXV; ++i) {
-      const int n = lane + i * 64;
-      const float d = n < C ? v[i] - mean : 0.0f;
-      q += d * d;
-    }
-    const float rstd = rsqrtf(wave_sum(q) / C + a.eps);
-#pragma unroll
-    for (int i = 0; i < MAXV; ++i) {
-      const int n = lane + i * 64;
-      if (n < C) v[i] = (v[i] - mean) * rstd * (1.0f + a.fin_sst[C + n] + a.t_emb[n]) + a.fin_sst[n] + a.t_emb[n];
-    }
-    float eps[16];
-#pragma unroll
-    for (int o = 0; o < 16; ++o) {
-      float acc = 0.0f;
-#pragma unroll
-      for (int i = 0; i < MAXV; ++i) {
-        const int n = lane + i * 64;
-        if (n < C) acc += v[i] * to_f<T>(wl[o * C + n]);
+      for (int q = 0; q < 8; ++q) {
+        sh[i][q] += t0[q];
+        sc[i][q] += t0[q];
       }
-      eps[o] = wave_sum(acc);
-    }
-    if (lane < 16) {
-      const int o = lane, pix = o >> 2, c = o & 3, pi = pix >> 1, qi = pix & 1;
-      float e = 0.0f;
+    } else {
 #pragma unroll
-      for (int k = 0; k < 16; ++k)
-        if (k == o) e = eps[k];
-      e += a.fin_b[pix * a.out_ch + c];
-      const int pk = a.rows[r];
-      const int b = row_chain(pk), tok = row_token(pk);
-      const int y = tok / a.gw, xx = tok - y * a.gw;
-      const int Hl = a.gh * 2, Wl = a.gw * 2;
-      const size_t li = (((size_t)b * 4 + c) * Hl + 2 * y + pi) * Wl + 2 * xx + qi;
-      const float xn = a.ca * a.latent_in[li] + a.cb * e;
-      a.latent_out[li] = xn;
-      if (a.traj_next) a.traj_next[b * a.traj_chain_stride + (li - (size_t)b * 4 * Hl * Wl)] = xn;
+      for (int q = 0; q < 8; ++q) v[i][q] = sh[i][q] = sc[i][q] = 0.0f;
     }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) s += v[i][q];
+  }
+  const float mean = wave_sum(s) / C;
+  float qs = 0.0f;
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i)
+    if (8 * (lane + 64 * i) < C)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const float d = v[i][q] - mean;
+        qs += d * d;
+      }
+  const float rstd = rsqrtf(wave_sum(qs) / C + a.eps);
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[i][q] = (v[i][q] - mean) * rstd * (1.0f + sc[i][q]) + sh[i][q];
+  float eps[16];
+#pragma unroll
+  for (int o = 0; o < 16; ++o) {
+    float acc = 0.0f;
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i) {
+      const int k0 = 8 * (lane + 64 * i);
+      if (k0 < C) {
+        float wv[8];
+        load8<T>(wl + (size_t)o * C + k0, wv);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc += v[i][q] * wv[q];
+      }
+    }
+    eps[o] = wave_sum(acc);
+  }
+  if (lane < 16) {
+    const int o = lane, pix = o >> 2, c = o & 3, pi = pix >> 1, qi = pix & 1;
+    float e = 0.0f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+      if (k == o) e = eps[k];
+    e += a.fin_b[pix * a.out_ch + c];
+    const int pk = a.rows[r];
+    const int b = row_chain(pk), tok = row_token(pk);
+    const int y = tok / a.gw, xx = tok - y * a.gw;
+    const int Hl = a.gh * 2, Wl = a.gw * 2;
+    const size_t li = (((size_t)b * 4 + c) * Hl + 2 * y + pi) * Wl + 2 * xx + qi;
+    const float xn = a.ca * a.latent_in[li] + a.cb * e;
+    a.latent_out[li] = xn;
+    if (a.traj_next) a.traj_next[b * a.traj_chain_stride + (li - (size_t)b * 4 * Hl * Wl)] = xn;
   }
 }
 
 template <typename T> hipError_t launch_final_ddim(const FinalArgs &a, hipStream_t s) {
   if (a.R <= 0) return hipSuccess;
-  if (a.C > 64 * 24 || a.out_ch < 4) return hipErrorInvalidValue;
+  if (a.C % 8 || a.C > 64 * 8 * 3 || a.out_ch < 4) return hipErrorInvalidValue;
   const size_t lds = (size_t)16 * a.C * sizeof(T);
   rc_launch(final_ddim_kernel<T>, dim3((a.R + FIN_ROWS - 1) / FIN_ROWS), dim3(256), lds, s, a);
   return hipGetLastError();
