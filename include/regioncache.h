@@ -132,8 +132,8 @@ typedef struct {
 
 /* The cache pool (Sec. 3.2): one caller-owned device buffer of
  * rc_cache_bytes(ctx, batch, steps) bytes holding, for every chain b, step t
- * and block l, a slot of three E arrays -- K [H][N][72], V transposed
- * [H][72][N] and the block-output hidden state H [N][C] -- followed (not in
+ * and block l, a slot of three E arrays -- K [H][N][72], V [H][N][72] and
+ * the block-output hidden state H [N][C] -- followed (not in
  * token mode) by the float32 latent trajectory [batch][steps+1][c][2gh][2gw],
  * where entry t is the latent entering step t and entry t+1 the latent it
  * produced.  rc_cache_offsets gives the byte offsets. */
@@ -175,11 +175,11 @@ size_t rc_text_kv_bytes(const rc_ctx *ctx, int32_t batch);
  * `batch` chains (a dense step uses batch*N rows). */
 size_t rc_workspace_bytes(const rc_ctx *ctx, int32_t max_rows, int32_t batch);
 
-/* Byte offsets inside the cache of slot (b, t, l): K, transposed V and H;
+/* Byte offsets inside the cache of slot (b, t, l): K, V and H;
  * and of latent trajectory entry (b, t) (returns RC_ERR_SHAPE in token mode
  * for the latent). */
 rc_status rc_cache_offsets(const rc_ctx *ctx, const rc_cache_view *cache, int32_t b, int32_t t,
-                           int32_t l, size_t *k_off, size_t *vt_off, size_t *h_off);
+                           int32_t l, size_t *k_off, size_t *v_off, size_t *h_off);
 rc_status rc_cache_latent_offset(const rc_ctx *ctx, const rc_cache_view *cache, int32_t b,
                                  int32_t t, size_t *off);
 

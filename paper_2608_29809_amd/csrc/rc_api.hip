@@ -355,7 +355,7 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
   for (int l = 0; l < L; ++l) {
     const rc_layer_weights &lw = c->layers[l];
     T *slot = (T *)(cb + slot_offset(c, T_, 0, step, l));
-    T *Ks = slot, *Vts = slot + kv_half, *Hs = slot + 2 * kv_half;
+    T *Ks = slot, *Vs = slot + kv_half, *Hs = slot + 2 * kv_half;
 
     if (!a1_ready)
       RC_TRY(timed(c, RC_KC_NORM, s, [&] { return rc::launch_ln_mod<T>(X, R, C, lw.sst, t0, 0, c->cfg.ln_eps, A1, s); }));
@@ -363,13 +363,13 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
     {  // QKV with the K/V scatter into the slot
       rc::GemmArgs g{};
       g.A = A1; g.W = lw.qkv_w; g.bias = lw.qkv_b; g.M = R; g.N = 3 * C; g.K = C; g.lda = C;
-      g.out = Q; g.ldo = C; g.rows = rows; g.kslot = Ks; g.vtslot = Vts;
+      g.out = Q; g.ldo = C; g.rows = rows; g.kslot = Ks; g.vslot = Vs;
       g.chain_stride = slot_chain_stride; g.tokens = N; g.hidden = C;
       RC_TRY(gemm<T>(c, RC_KC_GEMM_QKV, g, rc::EPI_QKV, gpart, gpf, s));
     }
     {  // region-level sparse self-attention over the whole slot
       rc::AttnArgs a{};
-      a.Q = Q; a.K = Ks; a.Vt = Vts; a.chain_stride = slot_chain_stride; a.head_stride = (long long)N * rc::kHeadDim;
+      a.Q = Q; a.K = Ks; a.V = Vs; a.v_rowmajor = 1; a.chain_stride = slot_chain_stride; a.head_stride = (long long)N * rc::kHeadDim;
       a.offsets = offsets_dev; a.n_keys = N; a.n_valid = N; a.hidden = C; a.splits = splits;
       a.O = O; a.Opart = part; a.ML = ml; a.total_rows = R; a.scale_log2 = scale_log2;
       RC_TRY(timed(c, RC_KC_ATTN_SELF, s, [&] {
@@ -396,7 +396,7 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
     {  // cross-attention to the text, emitting the delta-token maps
       const T *tkv = (const T *)io->text_kv + (size_t)l * B * text_kv_elems_per_entry(c);
       rc::AttnArgs a{};
-      a.Q = Q; a.K = tkv; a.Vt = tkv + (size_t)H * c->Mp * rc::kHeadDim;
+      a.Q = Q; a.K = tkv; a.V = tkv + (size_t)H * c->Mp * rc::kHeadDim; a.v_rowmajor = 0;
       a.chain_stride = (long long)text_kv_elems_per_entry(c); a.head_stride = (long long)c->Mp * rc::kHeadDim;
       a.offsets = offsets_dev; a.n_keys = c->Mp; a.n_valid = c->M; a.hidden = C; a.splits = 1;
       a.O = O; a.total_rows = R; a.scale_log2 = scale_log2;
@@ -593,14 +593,14 @@ size_t rc_workspace_bytes(const rc_ctx *c, int32_t max_rows, int32_t batch) {
 }
 
 rc_status rc_cache_offsets(const rc_ctx *c, const rc_cache_view *cache, int32_t b, int32_t t, int32_t l,
-                           size_t *k_off, size_t *vt_off, size_t *h_off) {
+                           size_t *k_off, size_t *v_off, size_t *h_off) {
   RC_CHECK(c && cache, RC_ERR_INVALID_ARG, "null argument");
   RC_CHECK(b >= 0 && b < cache->batch && t >= 0 && t < cache->steps && l >= 0 && l < c->L, RC_ERR_SHAPE,
            "slot (%d, %d, %d) out of range", b, t, l);
   const size_t base = slot_offset(c, cache->steps, b, t, l);
   const size_t half = (size_t)c->H * c->N * rc::kHeadDim * c->esz;
   if (k_off) *k_off = base;
-  if (vt_off) *vt_off = base + half;
+  if (v_off) *v_off = base + half;
   if (h_off) *h_off = base + 2 * half;
   return RC_OK;
 }

@@ -64,7 +64,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const int keys_per_split = a.n_keys / a.splits;
   const int kbeg = split * keys_per_split, kend = kbeg + keys_per_split;
   const T *Kg = (const T *)a.K + b * a.chain_stride + h * a.head_stride;
-  const T *Vg = (const T *)a.Vt + b * a.chain_stride + h * a.head_stride;
+  const T *Vg = (const T *)a.V + b * a.chain_stride + h * a.head_stride;
 
   // queries as the B operand of S^T = K Q^T
   frag qf[DC];
@@ -89,8 +89,13 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     for (int i = 0; i < V_IT; ++i) {
       const int ch = tid + i * 256;
       if (ch < V_CH) {
-        const int d = ch / V_CPR, c = ch % V_CPR;
-        rv[i] = *(const V16 *)(Vg + (size_t)d * a.n_keys + key0 + c * VE);
+        if (a.v_rowmajor) {  // chunk = VE consecutive dims of one key
+          const int key = ch / (D / VE), c = ch % (D / VE);
+          rv[i] = *(const V16 *)(Vg + (size_t)(key0 + key) * D + c * VE);
+        } else {             // chunk = VE consecutive keys of one dim
+          const int d = ch / V_CPR, c = ch % V_CPR;
+          rv[i] = *(const V16 *)(Vg + (size_t)d * a.n_keys + key0 + c * VE);
+        }
       }
     }
   };
@@ -104,8 +109,15 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     for (int i = 0; i < V_IT; ++i) {
       const int ch = tid + i * 256;
       if (ch < V_CH) {
-        const int d = ch / V_CPR, c = ch % V_CPR;
-        *(V16 *)(Vs + d * VT_LD + c * VE) = rv[i];
+        if (a.v_rowmajor) {  // transpose the chunk into the V^T tile
+          const int key = ch / (D / VE), c = ch % (D / VE);
+          const T *e = (const T *)&rv[i];
+#pragma unroll
+          for (int q = 0; q < VE; ++q) Vs[(c * VE + q) * VT_LD + key] = e[q];
+        } else {
+          const int d = ch / V_CPR, c = ch % V_CPR;
+          *(V16 *)(Vs + d * VT_LD + c * VE) = rv[i];
+        }
       }
     }
   };

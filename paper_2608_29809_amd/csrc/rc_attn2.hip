@@ -74,7 +74,7 @@ __global__ __launch_bounds__(256, 2) void attn2_kernel(AttnArgs a) {
   const int n_tiles = a.n_keys / A2_BK;
   const int t_beg = (int)((long)split * n_tiles / a.splits), t_end = (int)((long)(split + 1) * n_tiles / a.splits);
   const bf16 *Kg = (const bf16 *)a.K + b * a.chain_stride + h * a.head_stride;
-  const bf16 *Vg = (const bf16 *)a.Vt + b * a.chain_stride + h * a.head_stride;
+  const bf16 *Vg = (const bf16 *)a.V + b * a.chain_stride + h * a.head_stride;  // transposed [72][n_keys]
 
   auto issue = [&](int stage, int tile) {
     char *ks = lds + stage * STAGE, *vs = ks + KT_BYTES;
@@ -287,7 +287,7 @@ __global__ __launch_bounds__(256, 2) void attn2_kernel(AttnArgs a) {
 
 hipError_t launch_attention2(const AttnArgs &a, int n_chains, int max_rows, bool cross, hipStream_t s) {
   if (max_rows <= 0) return hipSuccess;
-  if (a.n_keys % A2_BK != 0 || a.splits < 1 || a.splits > a.n_keys / A2_BK) return hipErrorInvalidValue;
+  if (a.n_keys % A2_BK != 0 || a.splits < 1 || a.splits > a.n_keys / A2_BK || a.v_rowmajor) return hipErrorInvalidValue;
   dim3 grid((max_rows + A2_BQ - 1) / A2_BQ, (a.hidden / kHeadDim) * a.splits, n_chains);
   if (cross)
     rc_launch(attn2_kernel<true, 2>, grid, dim3(256), 0, s, a);

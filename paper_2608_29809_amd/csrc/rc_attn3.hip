@@ -11,7 +11,12 @@
 //
 // * a three-tile ring: while tile t's values are read and tile t+1's keys are
 //   read, tile t+2 streams in; one barrier per tile;
-// * the loop carries the scores of the next tile in registers.
+// * the loop carries the scores of the next tile in registers;
+// * values are stored token-major like the keys ([n_keys][72] per head), so
+//   a tile is one contiguous 9216-byte copy; the V^T operand fragments are
+//   assembled by LDS transpose reads (ds_read_b64_tr_b16: within a 16-lane
+//   group, lane i's k-th element is element i%4 of the 4-element chunk whose
+//   address lane 4k + i/4 supplied), two per fragment.
 #include "rc_common.h"
 #include "rc_launch.h"
 #include "rc_internal.h"
@@ -31,12 +36,16 @@ __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)
 __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
   constexpr int D = kHeadDim;
   constexpr int KT_BYTES = A3_BK * D * 2;  // K tile [64][72]
-  constexpr int VT_BYTES = D * A3_BK * 2;  // V^T tile [72][64]
+  constexpr int VT_BYTES = A3_BK * D * 2;  // V tile [64][72]
   constexpr int STAGE = KT_BYTES + VT_BYTES;
   constexpr int K_CH = KT_BYTES / 16;      // 576 16-byte chunks per operand tile
-  __shared__ __attribute__((aligned(1024))) char lds[A3_STAGES * STAGE + 128];
-  char *ones_row = lds + A3_STAGES * STAGE;
-  if (threadIdx.x < 8) *(V16 *)(ones_row + threadIdx.x * 16) = V16{{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u}};
+  __shared__ __attribute__((aligned(1024))) char lds[A3_STAGES * STAGE + 16];
+  // two 4-element chunks read in place of value dims >= 72: (1, 0, 0, 0), so
+  // that output row 72 of O^T accumulates sum_k P[k] -- the softmax
+  // denominator, with the same rounded probabilities as the numerator -- and
+  // zeros for the rows that are never stored
+  char *ones_chunk = lds + A3_STAGES * STAGE, *zero_chunk = ones_chunk + 8;
+  if (threadIdx.x == 0) *(V16 *)ones_chunk = V16{{0x00003F80u, 0u, 0u, 0u}};
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 5, r32 = lane & 31;
@@ -50,7 +59,7 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
   const int n_tiles = a.n_keys / A3_BK;
   const int t_beg = (int)((long)split * n_tiles / a.splits), t_end = (int)((long)(split + 1) * n_tiles / a.splits);
   const bf16 *Kg = (const bf16 *)a.K + b * a.chain_stride + h * a.head_stride;
-  const bf16 *Vg = (const bf16 *)a.Vt + b * a.chain_stride + h * a.head_stride;
+  const bf16 *Vg = (const bf16 *)a.V + b * a.chain_stride + h * a.head_stride;  // [n_keys][72]
 
   auto issue = [&](int stage, int tile) {
     char *ks = lds + stage * STAGE, *vs = ks + KT_BYTES;
@@ -63,15 +72,13 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
         __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)(kt + (base + lane) * 16),
                                          (__attribute__((address_space(3))) void *)(ks + base * 16), 16, 0, 0);
     }
+    const char *vt = (const char *)(Vg + (size_t)key0 * D);
 #pragma unroll
     for (int i = 0; i < 3; ++i) {
       const int base = i * 256 + wave * 64;
-      if (base < K_CH) {
-        const int ch = base + lane, d = ch >> 3, lc = (ch & 7) ^ (d & 7);
-        const bf16 *src = Vg + (size_t)d * a.n_keys + key0 + lc * 8;
-        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
+      if (base < K_CH)
+        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)(vt + (base + lane) * 16),
                                          (__attribute__((address_space(3))) void *)(vs + base * 16), 16, 0, 0);
-      }
     }
   };
   // the first two key tiles depend only on (chain, head, key range): they
@@ -126,6 +133,30 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
     for (int e = 0; e < 16; ++e) o[t][e] = 0.0f;
   float m_run = -INFINITY;
   const float c2 = a.scale_log2;
+
+  // Transpose reads of the V tile: the fragment of dims 32t + (lane%32) and
+  // keys kb..kb+7 (kb = st*32 + c*16 + g*8) is two reads; in the first this
+  // lane supplies the 4 dims from d0 of key kb_w + j/4, in the second of key
+  // kb_w + 4 + j/4 (16-lane group w = lane/16, j = lane%16).
+  const int tw = lane >> 4, tj = lane & 15;
+  int v_off[3];  // byte offset of the supplied chunk within a key row block, per dim block t
+#pragma unroll
+  for (int t = 0; t < 3; ++t) {
+    const int d0 = 32 * t + 16 * (tw & 1) + 4 * (tj & 3);
+    v_off[t] = ((tj >> 2) * D + d0) * 2;
+  }
+  const int d0_2 = 64 + 16 * (tw & 1) + 4 * (tj & 3);  // dims of the last block: real below 72
+  auto vfrag = [&](const char *vs, int kb, int t) {
+    typedef short v4s __attribute__((ext_vector_type(4)));
+    typedef short v8s __attribute__((ext_vector_type(8)));
+    const char *p0 = vs + kb * (D * 2) + v_off[t];
+    const char *p1 = p0 + 4 * D * 2;
+    if (t == 2 && d0_2 >= D) p0 = p1 = (d0_2 == D) ? ones_chunk : zero_chunk;
+    const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s *)p0);
+    const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s *)p1);
+    const v8s both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(bf16x8, both);
+  };
 
   // prologue: wait for tile t_beg (every load issued after its last one --
   // tile t_beg+1, the queries -- may still be in flight), scores of t_beg
@@ -211,16 +242,10 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
-        const int lc = st * 4 + c * 2 + g;
+        const int kb = st * 32 + c * 16 + (tw >> 1) * 8;  // keys of lane group g = tw/2
 #pragma unroll
-        for (int t = 0; t < 3; ++t) {
-          // rows d >= 72 feed output rows that are never stored: clamped reads
-          const int d = min(t * 32 + r32, D - 1);
-          const char *va = vs + d * 128 + ((lc ^ (d & 7)) << 4);
-          if (t == 2 && r32 == 8) va = ones_row + (lc << 4);
-          const bf16x8 vf = *(const bf16x8 *)va;
-          o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[st][c], o[t], 0, 0, 0);
-        }
+        for (int t = 0; t < 3; ++t)
+          o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(vs, kb, t), pf[st][c], o[t], 0, 0, 0);
       }
     if (HAS_NEXT) {
       s_cur[0] = s_next[0];
@@ -326,7 +351,8 @@ hipError_t launch_attn_combine_norm(const void *Opart, const float *ML, void *O,
 
 hipError_t launch_attention3(const AttnArgs &a, int n_chains, int max_rows, hipStream_t s) {
   if (max_rows <= 0) return hipSuccess;
-  if (a.n_keys % A3_BK != 0 || a.splits < 1 || a.splits > a.n_keys / A3_BK) return hipErrorInvalidValue;
+  if (a.n_keys % A3_BK != 0 || a.splits < 1 || a.splits > a.n_keys / A3_BK || !a.v_rowmajor)
+    return hipErrorInvalidValue;
   dim3 grid((max_rows + A3_BQ - 1) / A3_BQ, (a.hidden / kHeadDim) * a.splits, n_chains);
   rc_launch(attn3_kernel, grid, dim3(256), 0, s, a);
   return hipGetLastError();

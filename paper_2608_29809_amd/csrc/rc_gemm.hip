@@ -147,7 +147,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
             if (part == 1)
               ((T *)g.kslot)[cb + ((size_t)hh * g.tokens + tok) * kHeadDim + dd] = from_f<T>(v);
             else
-              ((T *)g.vtslot)[cb + ((size_t)hh * kHeadDim + dd) * g.tokens + tok] = from_f<T>(v);
+              ((T *)g.vslot)[cb + ((size_t)hh * g.tokens + tok) * kHeadDim + dd] = from_f<T>(v);
           }
         } else if (EPI == EPI_TEXTKV) {
           const int b = m / g.text_len, t = m - b * g.text_len;

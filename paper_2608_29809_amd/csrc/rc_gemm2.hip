@@ -63,10 +63,7 @@ __device__ __forceinline__ void epi_store(const GemmArgs &g, int m, int n, float
       const int pk = g.rows[m];
       const size_t cb = (size_t)row_chain(pk) * g.chain_stride;
       const int tok = row_token(pk);
-      if (part == 1)
-        ((bf16 *)g.kslot)[cb + ((size_t)hh * g.tokens + tok) * kHeadDim + dd] = (bf16)v;
-      else
-        ((bf16 *)g.vtslot)[cb + ((size_t)hh * kHeadDim + dd) * g.tokens + tok] = (bf16)v;
+      ((bf16 *)(part == 1 ? g.kslot : g.vslot))[cb + ((size_t)hh * g.tokens + tok) * kHeadDim + dd] = (bf16)v;
     }
   } else if (EPI == EPI_TEXTKV) {
     const int b = m / g.text_len, t = m - b * g.text_len;
@@ -114,7 +111,7 @@ __device__ __forceinline__ void resid4(const GemmArgs &g, int m, int n, float *v
 }
 
 // Four consecutive output columns n..n+3 of row m (n % 4 == 0; never the
-// transposed-V part, whose columns are handled one by one).
+// transposed text values, whose columns are handled one by one).
 template <int EPI>
 __device__ __forceinline__ void epi4(const GemmArgs &g, int m, int n, float *v, int part) {
   if (EPI == EPI_STORE) {
@@ -131,8 +128,8 @@ __device__ __forceinline__ void epi4(const GemmArgs &g, int m, int n, float *v, 
       st4((bf16 *)g.out + (size_t)m * g.ldo + n, v);
     } else {
       const int pk = g.rows[m];
-      const int c = n - g.hidden, hh = c / kHeadDim, dd = c - hh * kHeadDim;
-      st4((bf16 *)g.kslot + (size_t)row_chain(pk) * g.chain_stride +
+      const int c = n - part * g.hidden, hh = c / kHeadDim, dd = c - hh * kHeadDim;
+      st4((bf16 *)(part == 1 ? g.kslot : g.vslot) + (size_t)row_chain(pk) * g.chain_stride +
               ((size_t)hh * g.tokens + row_token(pk)) * kHeadDim + dd, v);
     }
   } else if (EPI == EPI_TEXTKV) {
@@ -309,7 +306,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
     return;
   }
   const int tile_part = (EPI == EPI_QKV || EPI == EPI_TEXTKV) ? n0 / g.hidden : 0;
-  const bool transposed = (EPI == EPI_QKV && tile_part == 2) || (EPI == EPI_TEXTKV && tile_part == 1);
+  const bool transposed = EPI == EPI_TEXTKV && tile_part == 1;
   if (!transposed) {
     for (int idx = tid; idx < BM * BN / 4; idx += NT) {
       const int row = idx / (BN / 4), c4 = (idx % (BN / 4)) * 4;
@@ -324,7 +321,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
     }
   } else {
     // a wave walks one column, lanes on consecutive rows: each store covers
-    // consecutive tokens of one transposed-V row
+    // consecutive text tokens of one transposed-V row
     static_assert(NT % BM == 0, "a pass must cover whole columns");
     for (int idx = tid; idx < BM * BN; idx += NT) {
       const int col = idx / BM, row = idx - col * BM;

@@ -10,7 +10,7 @@ enum GemmEpi {
   EPI_STORE = 0,   // out = E(acc + bias)
   EPI_GELU = 1,    // out = E(gelu_tanh(acc + bias))
   EPI_RESID = 2,   // X += gate * (acc + bias); optional E copies of X (xt, H slot scatter, hidden rows)
-  EPI_QKV = 3,     // q -> out (compact), k -> K slot, v -> transposed V slot
+  EPI_QKV = 3,     // q -> out (compact), k -> K slot, v -> V slot (token-major rows, like K)
   EPI_TEXTKV = 4,  // text keys/values -> per-chain text K / transposed V
 };
 
@@ -33,7 +33,7 @@ struct GemmArgs {
   const int *rows;    // packed (chain<<16)|token per row
   void *hslot;        // H of chain 0's slot, or null
   void *kslot;        // K of chain 0's slot
-  void *vtslot;       // transposed V of chain 0's slot
+  void *vslot;        // V of chain 0's slot (row-major like K)
   long long chain_stride;  // elements between consecutive chains' slots
   int tokens;              // N tokens per chain
   int hidden;              // C
@@ -46,8 +46,9 @@ struct GemmArgs {
 struct AttnArgs {
   const void *Q;         // [R][C] E compact queries (chains concatenated)
   const void *K;         // chain 0, head 0 keys [n_keys][72]
-  const void *Vt;        // chain 0, head 0 transposed values [72][n_keys]
-  long long chain_stride;  // elements between chains for K and Vt
+  const void *V;         // chain 0, head 0 values: [n_keys][72] (v_rowmajor) or transposed [72][n_keys]
+  int v_rowmajor;        // 1 for the cache's values, 0 for the transposed text values
+  long long chain_stride;  // elements between chains for K and V
   long long head_stride;   // elements between heads (n_keys*72)
   const int *offsets;    // [B+1] device row offsets of chains
   int n_keys;            // keys per chain (multiple of 64)

@@ -77,10 +77,10 @@ class CacheBuffer:
         m = self.model
         return self._typed(self.offsets(b, t, l)[0], m.H * m.N * 72, m.dtype).view(m.H, m.N, 72)
 
-    def Vt(self, b, t, l):
-        """Values of slot (b, t, l), transposed: [heads, 72, N]."""
+    def V(self, b, t, l):
+        """Values of slot (b, t, l) as [heads, N, 72] (token-major, like the keys)."""
         m = self.model
-        return self._typed(self.offsets(b, t, l)[1], m.H * m.N * 72, m.dtype).view(m.H, 72, m.N)
+        return self._typed(self.offsets(b, t, l)[1], m.H * m.N * 72, m.dtype).view(m.H, m.N, 72)
 
     def H(self, b, t, l):
         """Block-output hidden state of slot (b, t, l): [N, C]."""

@@ -48,12 +48,12 @@ def upload_slot(model, cache, t, slot):
     for l in range(L):
         for b in range(B):
             cache.K(b, t, l).copy_(model.to_storage(slot["K"][l, b]))
-            cache.Vt(b, t, l).copy_(model.to_storage(np.ascontiguousarray(slot["V"][l, b].transpose(0, 2, 1))))
+            cache.V(b, t, l).copy_(model.to_storage(slot["V"][l, b]))
             cache.H(b, t, l).copy_(model.to_storage(slot["H"][l, b]))
 
 
 def download_slot(cache, t, L, B):
     K = np.stack([np.stack([to_np(cache.K(b, t, l)) for b in range(B)]) for l in range(L)])
-    V = np.stack([np.stack([to_np(cache.Vt(b, t, l)).transpose(0, 2, 1) for b in range(B)]) for l in range(L)])
+    V = np.stack([np.stack([to_np(cache.V(b, t, l)) for b in range(B)]) for l in range(L)])
     H = np.stack([np.stack([to_np(cache.H(b, t, l)) for b in range(B)]) for l in range(L)])
     return dict(K=K, V=V, H=H)

@@ -309,14 +309,14 @@ def test_empty_mask_and_poison():
     idx = np.arange(200, 260)
     for l in range(s.layers):
         cache.K(0, 0, l)[:, idx] = float("nan")
-        cache.Vt(0, 0, l)[:, :, idx] = float("nan")
+        cache.V(0, 0, l)[:, idx] = float("nan")
         cache.H(0, 0, l)[idx] = float("nan")
     model.reuse_step(cache, 0, ActiveSet.from_lists([idx]), torch.from_numpy(lat).cuda(), 500, 450, tkv,
                      latent_out=out)
     torch.cuda.synchronize()
     for l in range(s.layers):
         assert torch.isfinite(cache.K(0, 0, l).float()).all()
-        assert torch.isfinite(cache.Vt(0, 0, l).float()).all()
+        assert torch.isfinite(cache.V(0, 0, l).float()).all()
         assert torch.isfinite(cache.H(0, 0, l).float()).all()
     assert torch.isfinite(out).all()
 
