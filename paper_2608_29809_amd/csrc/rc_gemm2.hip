@@ -167,7 +167,10 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
   constexpr int STAGE_BYTES = (BM + BN) * 128;
   constexpr int GROUP_BYTES = STAGES * STAGE_BYTES;  // one K group's ring
   constexpr int CLD = BN + 4;                         // row of an fp32 output tile in LDS
-  static_assert(BM * CLD * 4 <= GROUP_BYTES, "output tile must fit a group's ring");
+  // the fp32 output tile is staged through the rings in PASSES row bands
+  constexpr int PASSES = (BM * CLD * 4 <= GROUP_BYTES) ? 1 : 2;
+  constexpr int HB = BM / PASSES;
+  static_assert(HB * CLD * 4 <= GROUP_BYTES && HB % WM == 0, "an output band must fit a group's ring");
   __shared__ __attribute__((aligned(1024))) char lds[KG * GROUP_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -271,20 +274,11 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
   }
 
   // Each K group's tile goes to LDS (the rings are free: every load has been
-  // consumed); the groups' tiles are summed in group order while the tile is
-  // written back with 16-byte row-contiguous accesses.  Tiles of a
-  // transposed-V output are walked column-major instead so that consecutive
-  // threads write consecutive tokens.
-  __syncthreads();
+  // consumed), one band of HB rows at a time; the groups' tiles are summed in
+  // group order while the band is written back with 16-byte row-contiguous
+  // accesses.  Tiles of transposed text values are walked column-major
+  // instead so that consecutive threads write consecutive tokens.
   float *ct = (float *)ring;
-#pragma unroll
-  for (int j = 0; j < FN; ++j)
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int e = 0; e < 16; ++e)
-        ct[(wm * WM + i * 32 + (e >> 2) * 8 + g32 * 4 + (e & 3)) * CLD + wn * WN + j * 32 + r32] = acc[i][j][e];
-  __syncthreads();
   auto tile_at = [&](int row, int col) {
     float v = 0.0f;
 #pragma unroll
@@ -292,45 +286,59 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
     return v;
   };
   constexpr int NT = 64 * NW * KG;
-  if (SPLIT) {
-    float *P = partial + (size_t)kz * g.M * g.N;
-    for (int idx = tid; idx < BM * BN / 4; idx += NT) {
-      const int row = idx / (BN / 4), c4 = (idx % (BN / 4)) * 4;
-      const int m = m0 + row;
-      if (m >= g.M) continue;
-      f32x4 v;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) v[q] = tile_at(row, c4 + q);
-      *(f32x4 *)(P + (size_t)m * g.N + n0 + c4) = v;
-    }
-    return;
-  }
   const int tile_part = (EPI == EPI_QKV || EPI == EPI_TEXTKV) ? n0 / g.hidden : 0;
   const bool transposed = EPI == EPI_TEXTKV && tile_part == 1;
-  if (!transposed) {
-    for (int idx = tid; idx < BM * BN / 4; idx += NT) {
-      const int row = idx / (BN / 4), c4 = (idx % (BN / 4)) * 4;
-      const int m = m0 + row;
-      if (m >= g.M) continue;
-      const int n = n0 + c4;
-      const f32x4 bb = g.bias ? *(const f32x4 *)(g.bias + n) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-      float v[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) v[q] = tile_at(row, c4 + q) + bb[q];
-      epi4<EPI>(g, m, n, v, tile_part);
+  for (int pass = 0; pass < PASSES; ++pass) {
+    const int rb = pass * HB;  // first tile row of the band
+    __syncthreads();
+    if (wm * WM >= rb && wm * WM < rb + HB) {
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            ct[(wm * WM - rb + i * 32 + (e >> 2) * 8 + g32 * 4 + (e & 3)) * CLD + wn * WN + j * 32 + r32] =
+                acc[i][j][e];
     }
-  } else {
-    // a wave walks one column, lanes on consecutive rows: each store covers
-    // consecutive text tokens of one transposed-V row
-    static_assert(NT % BM == 0, "a pass must cover whole columns");
-    for (int idx = tid; idx < BM * BN; idx += NT) {
-      const int col = idx / BM, row = idx - col * BM;
-      const int m = m0 + row;
-      if (m >= g.M) continue;
-      const int n = n0 + col;
-      const float bn = g.bias ? g.bias[n] : 0.0f;
-      const int c = n - tile_part * g.hidden, hh = c / kHeadDim, dd = c - hh * kHeadDim;
-      epi_store<EPI>(g, m, n, tile_at(row, col) + bn, 1.0f, tile_part, hh, dd);
+    __syncthreads();
+    if (SPLIT) {
+      float *P = partial + (size_t)kz * g.M * g.N;
+      for (int idx = tid; idx < HB * BN / 4; idx += NT) {
+        const int row = idx / (BN / 4), c4 = (idx % (BN / 4)) * 4;
+        const int m = m0 + rb + row;
+        if (m >= g.M) continue;
+        f32x4 v;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] = tile_at(row, c4 + q);
+        *(f32x4 *)(P + (size_t)m * g.N + n0 + c4) = v;
+      }
+    } else if (!transposed) {
+      for (int idx = tid; idx < HB * BN / 4; idx += NT) {
+        const int row = idx / (BN / 4), c4 = (idx % (BN / 4)) * 4;
+        const int m = m0 + rb + row;
+        if (m >= g.M) continue;
+        const int n = n0 + c4;
+        const f32x4 bb = g.bias ? *(const f32x4 *)(g.bias + n) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        float v[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] = tile_at(row, c4 + q) + bb[q];
+        epi4<EPI>(g, m, n, v, tile_part);
+      }
+    } else {
+      // a wave walks one column, lanes on consecutive rows: each store covers
+      // consecutive text tokens of one transposed-V row
+      static_assert(NT % HB == 0, "a pass must cover whole columns");
+      for (int idx = tid; idx < HB * BN; idx += NT) {
+        const int col = idx / HB, row = idx - col * HB;
+        const int m = m0 + rb + row;
+        if (m >= g.M) continue;
+        const int n = n0 + col;
+        const float bn = g.bias ? g.bias[n] : 0.0f;
+        const int c = n - tile_part * g.hidden, hh = c / kHeadDim, dd = c - hh * kHeadDim;
+        epi_store<EPI>(g, m, n, tile_at(row, col) + bn, 1.0f, tile_part, hh, dd);
+      }
     }
   }
 }
@@ -461,7 +469,7 @@ static void launch_reduce(const GemmArgs &a, int epi, int splits, const float *p
 }
 
 // Choice of tile, K groups and split count for a shape, from sweeps on the
-// step's shapes with cold weights (412, 723 and 4096 rows; N in {1152, 3456,
+// step's shapes with cold weights (412 to 16384 rows; N in {1152, 3456,
 // 4608}; K in {1152, 4608}).  A K step costs roughly the same time whatever
 // the tile, so a workgroup's time is set by its K steps: when the grid is
 // small the rows are cut into 32-row tiles and K over two groups of waves in
@@ -485,6 +493,10 @@ GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats) {
     }
     return p;
   }
+  if (N >= 3072 && M >= 1536 && M <= 8192) {
+    p.bm = 128;  // wide outputs at a few thousand rows: 64x64 waves, two workgroups per CU
+    return p;
+  }
   if (nk % 2 == 0) {
     if (t32 <= 256) {
       p.bm = 32;
@@ -504,7 +516,8 @@ hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &pl, float *p
   if (a.M <= 0) return hipSuccess;
   if (pl.bn != 128 || a.N % 128 || a.K % (G2_BK * pl.splits * pl.kg)) return hipErrorInvalidValue;
   const bool split = pl.splits > 1;
-  // tile shapes: 64 rows = 2x2 waves of 32x64; 32 rows = 1x4 waves of 32x32
+  // tile shapes: 128 rows = 2x2 waves of 64x64; 64 rows = 2x2 waves of 32x64;
+  // 32 rows = 1x4 waves of 32x32
 #define RC_G2(BMV, KGV, STG, WM_, WN_)                                                       \
   {                                                                                          \
     if (split) launch_g2<BMV, 128, STG, KGV, WM_, WN_, true>(a, epi, pl.splits, partial, s); \
@@ -517,6 +530,7 @@ hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &pl, float *p
     case 3213: RC_G2(32, 1, 3, 1, 4) break;
     case 3223: RC_G2(32, 2, 3, 1, 4) break;
     case 3232: RC_G2(32, 3, 2, 1, 4) break;
+    case 12812: RC_G2(128, 1, 2, 2, 2) break;
     default: return hipErrorInvalidValue;
   }
 #undef RC_G2

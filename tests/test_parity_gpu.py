@@ -286,6 +286,32 @@ def test_dense_step_vs_oracle():
     assert torch.equal(out2, out) and torch.equal(maps2, maps)
 
 
+@pytest.mark.gpu
+@pytest.mark.timeout(300)
+def test_dense_step_two_chains():
+    """Dense step of two chains at 1024 tokens each: 2048 rows per GEMM (the
+    128-row tile plan for the wide projections), both chains vs the oracle."""
+    _say("dense step, two chains")
+    s = synth.ModelShape(layers=2, grid_h=32, grid_w=32, dtype="bf16")
+    W = synth.make_weights(s, seed=6, stress=True)
+    txt = synth.make_text(s, 2, 6)
+    lat = synth.make_latent(s, 2, 6)
+    model = RegionCacheModel(s, W)
+    cache = model.alloc_cache(2, 2)
+    tkv = model.prepare_text(model.to_storage(txt))
+    out = torch.empty(lat.shape, device="cuda")
+    model.build_cache(cache, 0, torch.from_numpy(lat).cuda(), 900, 850, tkv, latent_out=out)
+    torch.cuda.synchronize()
+    got = download_slot(cache, 0, s.layers, 2)
+    for b in range(2):
+        ref = O.dense_step(s, W, lat[b], 900, 850, oracle_text_kv(s, W, txt[b]))
+        for k in ("H", "K", "V"):
+            e = relerr(got[k][:, b], ref[k])
+            _say(b, k, e)
+            assert e < 2e-2
+        assert relerr(to_np(out)[b], ref["latent_next"]) < 2e-2
+
+
 def test_empty_mask_and_poison():
     """No active token: slot unchanged and latent = cached trajectory.  Then
     NaN in the stale cached rows of the active tokens never reaches an output."""
