@@ -13,7 +13,9 @@ embedding, 28 blocks with the fused K/V scatter and the merge into the cached
 hidden state, final layer, DDIM update of the active patches).  The line also
 reports the dense step, the speedup of reuse over dense, and the whole 20-step
 editing turn (text preparation, 4 dense steps with map emission, edit-region
-localisation, 16 reuse steps) against an all-dense turn.
+localisation, 16 reuse steps) against an all-dense turn; without --quick also
+the 1024 px localisation read-out from raw logits, a batch-4 active-fraction
+sweep and a 512/1024/2048 px resolution sweep.
 
 Prints ONE JSON line.  `--gpus` above 1 is not supported (single-GPU build).
 """
@@ -245,11 +247,13 @@ def main():
     # ---------------------------------------------------------------- localisation workload
     loc = None
     sweep = None
+    res = None
     if not args.quick:
         loc = localize_leg(args)
         del cache
         torch.cuda.empty_cache()
         sweep = sweep_leg(model, args)
+        res = resolution_leg(W, args)
 
     # ---------------------------------------------------------------- oracle on the host cores
     cpu = None
@@ -284,6 +288,7 @@ def main():
         "roofline": roofline,
         "localize": loc,
         "fraction_sweep": sweep,
+        "resolution_sweep": res,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
@@ -326,6 +331,47 @@ def localize_leg(args):
     return dict(workload="logits bf16 [28,16,4096,120], 6 delta columns", maps_us=round(t_maps * 1000, 2),
                 logits_gbs=round(gbs, 1), hbm_frac=round(gbs / PEAK_HBM_GBS, 4),
                 mask_and_compaction_us=round(t_loc * 1000, 2), active_tokens=int(act.total))
+
+
+def resolution_leg(W, args):
+    """One chain at 512, 1024 and 2048 px (32x32, 64x64, 128x128 tokens), the
+    28-block model (same weights, position table of the grid), a seeded
+    15 % blob region: reuse-step and dense-step times."""
+    import dataclasses
+    import torch
+    import synth
+    from paper_2608_29809_amd.runtime import ActiveSet, RegionCacheModel
+    out = {}
+    for px, g in ((512, 32), (1024, 64), (2048, 128)):
+        shape = dataclasses.replace(synth.shape_c3(), grid_h=g, grid_w=g)
+        model = RegionCacheModel(shape, W)
+        cache = model.alloc_cache(1, 2)
+        txt = synth.make_text(shape, 1, args.seed + 2)
+        tkv = model.prepare_text(model.to_storage(txt))
+        lat = torch.from_numpy(synth.make_latent(shape, 1, args.seed + 2)).cuda()
+        nxt = torch.empty_like(lat)
+        rng = np.random.default_rng([args.seed, px])
+        act = ActiveSet.from_lists([np.flatnonzero(synth.blob_mask(g, g, 0.15, 2, rng))])
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+
+        def timed(fn, n=6):
+            fn()
+            torch.cuda.synchronize()
+            ev[0].record()
+            for _ in range(n):
+                fn()
+            ev[1].record()
+            torch.cuda.synchronize()
+            return ev[0].elapsed_time(ev[1]) / n
+
+        dense_ms = timed(lambda: model.build_cache(cache, 0, lat, 842, 789, tkv, latent_out=nxt))
+        reuse_ms = timed(lambda: model.reuse_step(cache, 0, act, lat, 842, 789, tkv, latent_out=nxt))
+        out[f"{px}px"] = dict(tokens=g * g, active=int(act.total), reuse_step_ms=round(reuse_ms, 3),
+                              dense_step_ms=round(dense_ms, 3), speedup=round(dense_ms / reuse_ms, 3))
+        log(f"{px} px: {g * g} tokens, {act.total} active: reuse {reuse_ms:.3f} ms, dense {dense_ms:.3f} ms")
+        del cache, model
+        torch.cuda.empty_cache()
+    return out
 
 
 def sweep_leg(model1, args):

@@ -365,3 +365,16 @@ def test_c3_reuse_step_full_size():
     idx = np.flatnonzero(synth.blob_mask(64, 64, 0.15, 2, np.random.default_rng(0)))
     got, refs, ctx = _reuse_case(s, 0, [idx], t=842, t_next=789)
     _check_reuse(s, got, refs, [idx], ctx)
+
+
+@pytest.mark.gpu
+@pytest.mark.timeout(400)
+def test_reuse_step_2048px():
+    """2048 px (128 x 128 = 16384 tokens), two blocks, a 10 % blob region: the
+    largest grid the library takes, keys of all 16384 tokens per head."""
+    _say("2048 px reuse")
+    s = synth.ModelShape(layers=2, grid_h=128, grid_w=128, dtype="bf16")
+    idx = np.flatnonzero(synth.blob_mask(128, 128, 0.10, 2, np.random.default_rng(3)))
+    got, refs, ctx = _reuse_case(s, 3, [idx], t=600, t_next=550)
+    _check_reuse(s, got, refs, [idx], ctx)
+
