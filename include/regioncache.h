@@ -203,7 +203,13 @@ rc_status rc_prepare_text(rc_ctx *ctx, const void *txt, int32_t batch, void *tex
  *              ADDS, for every computed token, the sum over heads and blocks
  *              of its cross-attention probability on each delta column into
  *              maps [batch][N][n_delta] (device float32).
- *   latent_out -- device float32 [batch][c][2gh][2gw] (NULL in token mode). */
+ *   latent_out -- device float32 [batch][c][2gh][2gw] (NULL in token mode).
+ *   text_valid -- device int32 [batch]: the number of valid (unpadded)
+ *              prompt tokens of each chain; cross-attention of chain b sees
+ *              text tokens 0 .. text_valid[b]-1 only (values are clamped to
+ *              1 .. text_len; delta columns of a chain should be valid
+ *              tokens, others get probability 0).  NULL: all text_len
+ *              tokens are valid. */
 typedef struct {
   const void *input;
   const float *t_vec;
@@ -213,6 +219,7 @@ typedef struct {
   int32_t n_delta;
   float *maps;
   float *latent_out;
+  const int32_t *text_valid;
 } rc_step_io;
 
 /* BUILD CACHE (Sec. 3.2): dense step `step` over every token of every chain.

@@ -398,7 +398,8 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       rc::AttnArgs a{};
       a.Q = Q; a.K = tkv; a.V = tkv + (size_t)H * c->Mp * rc::kHeadDim; a.v_rowmajor = 0;
       a.chain_stride = (long long)text_kv_elems_per_entry(c); a.head_stride = (long long)c->Mp * rc::kHeadDim;
-      a.offsets = offsets_dev; a.n_keys = c->Mp; a.n_valid = c->M; a.hidden = C; a.splits = 1;
+      a.offsets = offsets_dev; a.n_keys = c->Mp; a.n_valid = c->M; a.text_valid = io->text_valid;
+      a.hidden = C; a.splits = 1;
       a.O = O; a.total_rows = R; a.scale_log2 = scale_log2;
       if (emit) {
         a.n_delta = io->n_delta;

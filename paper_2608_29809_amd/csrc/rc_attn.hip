@@ -60,6 +60,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   if (q0 >= r1) return;  // uniform across the workgroup
   const int my_q = q0 + wave * 32 + (lane & 31);
   const bool q_ok = my_q < r1;
+  // keys of this chain that are valid (prompt padding masked)
+  const int nv = a.text_valid ? min(max(a.text_valid[b], 1), a.n_valid) : a.n_valid;
 
   const int keys_per_split = a.n_keys / a.splits;
   const int kbeg = split * keys_per_split, kend = kbeg + keys_per_split;
@@ -160,7 +162,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
       for (int e = 0; e < 16; ++e) {
         const int key = key0 + st * 32 + g * 16 + e;
         float x = s[st][e] * a.scale_log2;
-        if (key >= a.n_valid) x = -INFINITY;
+        if (key >= nv) x = -INFINITY;
         s[st][e] = x;
         tmax = fmaxf(tmax, x);
       }

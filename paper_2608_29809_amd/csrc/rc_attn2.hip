@@ -113,6 +113,8 @@ __global__ __launch_bounds__(256, 2) void attn2_kernel(AttnArgs a) {
   }
   const int my_q = q0 + wave * 32 + r32;
   const bool q_ok = my_q < r1;
+  // keys of this chain that are valid (prompt padding masked)
+  const int nv = a.text_valid ? min(max(a.text_valid[b], 1), a.n_valid) : a.n_valid;
 
   bf16x8 qf[5];
   {
@@ -179,7 +181,7 @@ __global__ __launch_bounds__(256, 2) void attn2_kernel(AttnArgs a) {
       for (int e = 0; e < 16; ++e) {
         if (CROSS) {
           const int key = key0 + st * 32 + (e >> 3) * 16 + g * 8 + (e & 7);
-          if (key >= a.n_valid) s[st][e] = -INFINITY;
+          if (key >= nv) s[st][e] = -INFINITY;
         }
         tmax = fmaxf(tmax, s[st][e]);
       }

@@ -53,6 +53,7 @@ struct AttnArgs {
   const int *offsets;    // [B+1] device row offsets of chains
   int n_keys;            // keys per chain (multiple of 64)
   int n_valid;           // keys >= n_valid are masked out
+  const int *text_valid; // device [chains] per-chain valid key counts (clamped to 1..n_valid), or null
   int hidden;            // C = heads*72
   int splits;            // key-range splits (grid.y = heads*splits)
   void *O;               // [R][C] E output (splits == 1)

@@ -169,7 +169,7 @@ class RegionCacheModel:
         abi.rc_prepare_text(self.ctx, _ptr(txt), B, _ptr(tkv), _ptr(ws), ws.numel(), _stream())
         return tkv
 
-    def _io(self, inp, timestep, timestep_next, tkv, delta, maps, latent_out, t_vec):
+    def _io(self, inp, timestep, timestep_next, tkv, delta, maps, latent_out, t_vec, text_valid=None):
         d = None
         n_delta = 0
         if delta is not None and len(delta):
@@ -179,19 +179,21 @@ class RegionCacheModel:
                             int(timestep_next), tkv.data_ptr(),
                             None if d is None else C.cast(d, C.POINTER(C.c_int32)), n_delta,
                             None if maps is None else maps.data_ptr(),
-                            None if latent_out is None else latent_out.data_ptr())
+                            None if latent_out is None else latent_out.data_ptr(),
+                            None if text_valid is None else text_valid.data_ptr())
         return io, d
 
     def build_cache(self, cache: CacheBuffer, step: int, inp: torch.Tensor, timestep: int, timestep_next: int,
-                    tkv: torch.Tensor, delta=None, maps=None, latent_out=None, t_vec=None):
-        io, keep = self._io(inp, timestep, timestep_next, tkv, delta, maps, latent_out, t_vec)
+                    tkv: torch.Tensor, delta=None, maps=None, latent_out=None, t_vec=None, text_valid=None):
+        """text_valid: optional device int32 [batch] of unpadded prompt lengths."""
+        io, keep = self._io(inp, timestep, timestep_next, tkv, delta, maps, latent_out, t_vec, text_valid)
         ws = self.workspace(cache.batch * self.N, cache.batch)
         abi.rc_build_cache(self.ctx, C.byref(cache.view), step, C.byref(io), _ptr(ws), ws.numel(), _stream())
 
     def reuse_step(self, cache: CacheBuffer, step: int, act: ActiveSet, inp: torch.Tensor, timestep: int,
                    timestep_next: int, tkv: torch.Tensor, delta=None, maps=None, latent_out=None, t_vec=None,
-                   fuse: bool = True, active_hidden: Optional[torch.Tensor] = None):
-        io, keep = self._io(inp, timestep, timestep_next, tkv, delta, maps, latent_out, t_vec)
+                   fuse: bool = True, active_hidden: Optional[torch.Tensor] = None, text_valid=None):
+        io, keep = self._io(inp, timestep, timestep_next, tkv, delta, maps, latent_out, t_vec, text_valid)
         ws = self.workspace(max(act.total, 1), cache.batch)
         s = act.struct()
         abi.rc_reuse_step(self.ctx, C.byref(cache.view), step, C.byref(s), C.byref(io), _ptr(active_hidden),

@@ -106,7 +106,7 @@ def test_buffer_sizes(ctx):
 
 def _io(**over):
     d = dict(input=FAKE, t_vec=None, timestep=500, timestep_next=450, text_kv=FAKE, delta_cols_host=None,
-             n_delta=0, maps=None, latent_out=FAKE)
+             n_delta=0, maps=None, latent_out=FAKE, text_valid=None)
     d.update(over)
     return abi.rc_step_io(*[d[f] for f, _ in abi.rc_step_io._fields_])
 

@@ -378,3 +378,62 @@ def test_reuse_step_2048px():
     got, refs, ctx = _reuse_case(s, 3, [idx], t=600, t_next=550)
     _check_reuse(s, got, refs, [idx], ctx)
 
+
+@pytest.mark.gpu
+@pytest.mark.timeout(300)
+def test_padded_prompts_per_chain():
+    """Prompts of different lengths in one batch (padding masked per chain):
+    the reuse step and the dense step equal the oracle run on each chain's
+    unpadded prompt, maps included."""
+    _say("padded prompts")
+    s = synth.ModelShape(layers=2, grid_h=32, grid_w=32, dtype="bf16")
+    W = weights(s, 8, True)
+    B, valid, delta = 3, [57, 120, 1], (0, 17, 40)
+    txt = synth.make_text(s, B, 8)
+    lat = synth.make_latent(s, B, 8)
+    lat_next_cached = synth.make_latent(s, B, 8, stream=77)
+    slot = synth.make_cache_slot(s, B, 8)
+    model = RegionCacheModel(s, W)
+    cache = model.alloc_cache(B, 2)
+    upload_slot(model, cache, 1, slot)
+    for b in range(B):
+        cache.latent(b, 2).copy_(torch.from_numpy(lat_next_cached[b]))
+    tkv = model.prepare_text(model.to_storage(txt))
+    tv = torch.tensor(valid, dtype=torch.int32, device="cuda")
+    rng = np.random.default_rng(8)
+    per = [np.sort(rng.choice(s.tokens, n, replace=False)) for n in (150, 64, 300)]
+    act = ActiveSet.from_lists(per)
+    maps = torch.zeros((B, s.tokens, len(delta)), device="cuda")
+    out = torch.empty(lat.shape, device="cuda")
+    model.reuse_step(cache, 1, act, torch.from_numpy(lat).cuda(), 500, 450, tkv, list(delta), maps, out,
+                     text_valid=tv)
+    torch.cuda.synchronize()
+    got = download_slot(cache, 1, s.layers, B)
+    for b in range(B):
+        L = valid[b]
+        tkv_o = oracle_text_kv(s, W, txt[b][:L])
+        d_ok = [d for d in delta if d < L]
+        cs = dict(K=slot["K"][:, b], V=slot["V"][:, b], H=slot["H"][:, b])
+        ref = O.reuse_step(s, W, lat[b], 500, 450, tkv_o, per[b], cs, lat_next_cached[b], np.array(d_ok))
+        for k in ("H", "K", "V"):
+            e = relerr(got[k][:, b][:, per[b]] if k == "H" else got[k][:, b][:, :, per[b]],
+                       ref[k][:, per[b]] if k == "H" else ref[k][:, :, per[b]])
+            _say(b, L, k, e)
+            assert e < 2e-2
+        assert relerr(to_np(out)[b], ref["latent_next"]) < 2e-2
+        m = to_np(maps)[b]
+        for j, d in enumerate(delta):
+            if d < L:
+                assert relerr(m[per[b], j], ref["maps"][per[b], d_ok.index(d)]) < 2e-2
+            else:
+                assert np.all(m[:, j] == 0.0)
+    # dense step, same prompts
+    out2 = torch.empty_like(out)
+    model.build_cache(cache, 0, torch.from_numpy(lat).cuda(), 700, 650, tkv, latent_out=out2, text_valid=tv)
+    torch.cuda.synchronize()
+    got = download_slot(cache, 0, s.layers, B)
+    for b in range(B):
+        ref = O.dense_step(s, W, lat[b], 700, 650, oracle_text_kv(s, W, txt[b][:valid[b]]))
+        assert relerr(got["H"][:, b], ref["H"]) < 2e-2
+        assert relerr(to_np(out2)[b], ref["latent_next"]) < 2e-2
+
