@@ -209,7 +209,16 @@ rc_status rc_prepare_text(rc_ctx *ctx, const void *txt, int32_t batch, void *tex
  *              text tokens 0 .. text_valid[b]-1 only (values are clamped to
  *              1 .. text_len; delta columns of a chain should be valid
  *              tokens, others get probability 0).  NULL: all text_len
- *              tokens are valid. */
+ *              tokens are valid.
+ *   guided, guidance_scale -- classifier-free guidance (not in the paper;
+ *              PixArt-alpha's sampling practice).  guided = 1: the batch holds
+ *              pairs of chains, 2p conditional and 2p+1 unconditional (null
+ *              prompt), with the same input latent, the same trajectory and
+ *              the same active tokens (equal counts are checked; equal
+ *              indices are the caller's promise).  The noise prediction of
+ *              each token is eps_u + guidance_scale * (eps_c - eps_u) and both
+ *              chains of a pair receive the same DDIM update.  guided = 0:
+ *              chains are independent. */
 typedef struct {
   const void *input;
   const float *t_vec;
@@ -220,6 +229,8 @@ typedef struct {
   float *maps;
   float *latent_out;
   const int32_t *text_valid;
+  int32_t guided;
+  float guidance_scale;
 } rc_step_io;
 
 /* BUILD CACHE (Sec. 3.2): dense step `step` over every token of every chain.

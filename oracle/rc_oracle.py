@@ -33,7 +33,7 @@ __all__ = [
     "text_kv", "cross_and_mlp", "block_dense", "block_reuse", "latent_to_patches", "patches_to_latent", "final_layer", "eps_from_output",
     "alphas_cumprod", "ddim_update", "dense_step", "reuse_step",
     "dense_block_tokens", "reuse_block_tokens", "maps_from_logits", "dilate",
-    "compact", "localize", "cosine_similarity", "reuse_cutoff", "step_plan",
+    "compact", "localize", "cosine_similarity", "reuse_cutoff", "step_plan", "guided_noise", "guided_latent",
 ]
 
 LN_EPS = 1e-6
@@ -371,6 +371,28 @@ def reuse_step(shape, W, latent, t: int, t_next: int, textKV, idx, cache,
         lat_next[idx] = ddim_update(x_patches, eps, a_t, a_n)
     return dict(K=np.stack(Ks), V=np.stack(Vs), H=np.stack(Hs), X=X,
                 latent_next=patches_to_latent(lat_next, s.grid_h, s.grid_w), maps=maps, eps=eps)
+
+
+def guided_noise(eps_cond, eps_uncond, scale: float):
+    """Classifier-free guidance of PixArt-alpha's sampler (not part of the
+    method): eps_u + scale (eps_c - eps_u)."""
+    return eps_uncond + scale * (eps_cond - eps_uncond)
+
+
+def guided_latent(shape, latent, latent_cached_next, idx, eps_cond, eps_uncond, scale: float, t: int,
+                  t_next: int, dt=np.float64):
+    """Latent after one guided step of the tokens `idx`: their patches take the
+    DDIM update with the guided noise of the two branches' predictions
+    (eps [R, c, p, p] from reuse_step or dense_step); the other patches take
+    the cached trajectory's next latent."""
+    p = shape.patch
+    idx = np.asarray(idx, dtype=np.int64)
+    a_t, a_n = _abar_pair(t, t_next)
+    lat_next = latent_to_patches(_f(latent_cached_next, dt), p).copy()
+    if idx.size:
+        x = latent_to_patches(_f(latent, dt), p)[idx]
+        lat_next[idx] = ddim_update(x, guided_noise(eps_cond, eps_uncond, scale), a_t, a_n)
+    return patches_to_latent(lat_next, shape.grid_h, shape.grid_w)
 
 
 def _token_mode_mod(W, t_vec, dt):

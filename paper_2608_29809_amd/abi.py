@@ -70,7 +70,8 @@ class rc_step_io(C.Structure):
     _fields_ = [("input", C.c_void_p), ("t_vec", C.c_void_p), ("timestep", C.c_int32),
                 ("timestep_next", C.c_int32), ("text_kv", C.c_void_p),
                 ("delta_cols_host", C.POINTER(C.c_int32)), ("n_delta", C.c_int32), ("maps", C.c_void_p),
-                ("latent_out", C.c_void_p), ("text_valid", C.c_void_p)]
+                ("latent_out", C.c_void_p), ("text_valid", C.c_void_p), ("guided", C.c_int32),
+                ("guidance_scale", C.c_float)]
 
 
 def _load():

@@ -207,6 +207,24 @@ rc_status check_io(const rc_ctx *c, const rc_step_io *io) {
     RC_CHECK(io->timestep_next >= -1 && io->timestep_next < 1000, RC_ERR_INVALID_ARG,
              "timestep_next %d outside [-1, 1000)", io->timestep_next);
   }
+  RC_CHECK(io->guided == 0 || io->guided == 1, RC_ERR_INVALID_ARG, "guided must be 0 or 1");
+  RC_CHECK(!io->guided || !c->cfg.token_mode, RC_ERR_UNSUPPORTED, "guidance needs the latent path");
+  RC_CHECK(!io->guided || std::isfinite(io->guidance_scale), RC_ERR_INVALID_ARG, "guidance_scale not finite");
+  return RC_OK;
+}
+
+// A guided step pairs chains 2p (conditional) and 2p+1 (unconditional) row
+// by row: the batch must be even and each pair's active counts equal.
+rc_status check_guided(const rc_step_io *io, int batch, const rc_active_set *act) {
+  if (!io->guided) return RC_OK;
+  RC_CHECK(batch % 2 == 0, RC_ERR_SHAPE, "guided step needs (conditional, unconditional) chain pairs, batch %d",
+           batch);
+  if (act)
+    for (int b = 0; b < batch; b += 2) {
+      const int n0 = act->offsets_host[b + 1] - act->offsets_host[b];
+      const int n1 = act->offsets_host[b + 2] - act->offsets_host[b + 1];
+      RC_CHECK(n0 == n1, RC_ERR_INDEX, "guided pair %d: %d and %d active tokens", b / 2, n0, n1);
+    }
   return RC_OK;
 }
 
@@ -459,6 +477,7 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
     fa.out_ch = c->cfg.out_ch; fa.eps = c->cfg.ln_eps; fa.fin_w = W.fin_w; fa.fin_b = W.fin_b;
     fa.fin_sst = W.fin_sst; fa.t_emb = temb; fa.latent_in = (const float *)io->input;
     fa.latent_out = io->latent_out; fa.traj_next = traj_next; fa.traj_chain_stride = lat_chain_stride;
+    fa.offsets = offsets_dev; fa.guided = io->guided; fa.gscale = io->guidance_scale;
     fa.ca = (float)(std::sqrt(an) / std::sqrt(at));
     fa.cb = (float)(std::sqrt(1.0 - an) - std::sqrt(an) * std::sqrt(1.0 - at) / std::sqrt(at));
     RC_TRY(timed(c, RC_KC_FINAL, s, [&] { return rc::launch_final_ddim<T>(fa, s); }));
@@ -633,6 +652,7 @@ rc_status rc_build_cache(rc_ctx *c, const rc_cache_view *cache, int32_t step, co
   RC_CHECK(c, RC_ERR_INVALID_ARG, "ctx is null");
   RC_TRY(check_cache(c, cache, step));
   RC_TRY(check_io(c, io));
+  RC_TRY(check_guided(io, cache->batch, nullptr));
   RC_CHECK((long)cache->batch * c->N <= (1L << 30), RC_ERR_SHAPE, "batch too large");
   RC_CHECK(device_present(), RC_ERR_NO_DEVICE, "no HIP device");
   hipStream_t s = (hipStream_t)stream;
@@ -662,6 +682,7 @@ rc_status rc_reuse_step(rc_ctx *c, const rc_cache_view *cache, int32_t step, con
   RC_TRY(check_cache(c, cache, step));
   RC_TRY(check_io(c, io));
   RC_TRY(check_active(c, cache, active));
+  RC_TRY(check_guided(io, cache->batch, active));
   RC_CHECK((flags & ~RC_FUSE_UPDATE) == 0, RC_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
   RC_CHECK(device_present(), RC_ERR_NO_DEVICE, "no HIP device");
   hipStream_t s = (hipStream_t)stream;

@@ -33,6 +33,11 @@ struct FinalArgs {
   float *traj_next;        // chain 0's trajectory entry t+1, or null
   long long traj_chain_stride;  // floats between chains' entries
   float ca, cb;            // DDIM: x' = ca*x + cb*eps
+  // classifier-free guidance: chains 2p (conditional) and 2p+1
+  // (unconditional) are paired row by row through the row offsets
+  const int *offsets;      // [B+1] device row offsets (guided only)
+  int guided;
+  float gscale;
 };
 
 hipError_t launch_build_rows(const int *offsets, const int *idx, int B, int R, int *rows, hipStream_t s);

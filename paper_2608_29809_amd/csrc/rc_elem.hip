@@ -256,62 +256,80 @@ __global__ __launch_bounds__(256) void final_ddim_kernel(FinalArgs a) {
   __syncthreads();
   const int r = blockIdx.x * FIN_ROWS + wave;
   if (r >= a.R) return;
-  // lane chunk i holds inputs 8*(lane + 64 i) .. +8 (C % 8 == 0, C <= 1536)
-  constexpr int MAXC = 3;
-  const float *x = a.X + (size_t)r * C;
-  float v[MAXC][8], sh[MAXC][8], sc[MAXC][8];
-  float s = 0.0f;
-#pragma unroll
-  for (int i = 0; i < MAXC; ++i) {
-    const int k0 = 8 * (lane + 64 * i);
-    if (k0 < C) {
-      float t0[8];
-      load8<float>(x + k0, v[i]);
-      load8<float>(a.fin_sst + k0, sh[i]);
-      load8<float>(a.fin_sst + C + k0, sc[i]);
-      load8<float>(a.t_emb + k0, t0);
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        sh[i][q] += t0[q];
-        sc[i][q] += t0[q];
-      }
-    } else {
-#pragma unroll
-      for (int q = 0; q < 8; ++q) v[i][q] = sh[i][q] = sc[i][q] = 0.0f;
-    }
-#pragma unroll
-    for (int q = 0; q < 8; ++q) s += v[i][q];
+  // guided: the wave of a conditional row also takes the unconditional row
+  // of the same token (same position in the paired chain); waves of
+  // unconditional rows have nothing to do
+  int r_u = -1;
+  if (a.guided) {
+    const int b = row_chain(a.rows[r]);
+    if (b & 1) return;
+    r_u = r + (a.offsets[b + 1] - a.offsets[b]);
   }
-  const float mean = wave_sum(s) / C;
-  float qs = 0.0f;
-#pragma unroll
-  for (int i = 0; i < MAXC; ++i)
-    if (8 * (lane + 64 * i) < C)
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const float d = v[i][q] - mean;
-        qs += d * d;
-      }
-  const float rstd = rsqrtf(wave_sum(qs) / C + a.eps);
-#pragma unroll
-  for (int i = 0; i < MAXC; ++i)
-#pragma unroll
-    for (int q = 0; q < 8; ++q) v[i][q] = (v[i][q] - mean) * rstd * (1.0f + sc[i][q]) + sh[i][q];
   float eps[16];
-#pragma unroll
-  for (int o = 0; o < 16; ++o) {
-    float acc = 0.0f;
-#pragma unroll
+  auto noise = [&](int row, float *e16) {
+    // lane chunk i holds inputs 8*(lane + 64 i) .. +8 (C % 8 == 0, C <= 1536)
+    constexpr int MAXC = 3;
+    const float *x = a.X + (size_t)row * C;
+    float v[MAXC][8], sh[MAXC][8], sc[MAXC][8];
+    float s = 0.0f;
+  #pragma unroll
     for (int i = 0; i < MAXC; ++i) {
       const int k0 = 8 * (lane + 64 * i);
       if (k0 < C) {
-        float wv[8];
-        load8<T>(wl + (size_t)o * C + k0, wv);
-#pragma unroll
-        for (int q = 0; q < 8; ++q) acc += v[i][q] * wv[q];
+        float t0[8];
+        load8<float>(x + k0, v[i]);
+        load8<float>(a.fin_sst + k0, sh[i]);
+        load8<float>(a.fin_sst + C + k0, sc[i]);
+        load8<float>(a.t_emb + k0, t0);
+  #pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          sh[i][q] += t0[q];
+          sc[i][q] += t0[q];
+        }
+      } else {
+  #pragma unroll
+        for (int q = 0; q < 8; ++q) v[i][q] = sh[i][q] = sc[i][q] = 0.0f;
       }
+  #pragma unroll
+      for (int q = 0; q < 8; ++q) s += v[i][q];
     }
-    eps[o] = wave_sum(acc);
+    const float mean = wave_sum(s) / C;
+    float qs = 0.0f;
+  #pragma unroll
+    for (int i = 0; i < MAXC; ++i)
+      if (8 * (lane + 64 * i) < C)
+  #pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const float d = v[i][q] - mean;
+          qs += d * d;
+        }
+    const float rstd = rsqrtf(wave_sum(qs) / C + a.eps);
+  #pragma unroll
+    for (int i = 0; i < MAXC; ++i)
+  #pragma unroll
+      for (int q = 0; q < 8; ++q) v[i][q] = (v[i][q] - mean) * rstd * (1.0f + sc[i][q]) + sh[i][q];
+  #pragma unroll
+    for (int o = 0; o < 16; ++o) {
+      float acc = 0.0f;
+  #pragma unroll
+      for (int i = 0; i < MAXC; ++i) {
+        const int k0 = 8 * (lane + 64 * i);
+        if (k0 < C) {
+          float wv[8];
+          load8<T>(wl + (size_t)o * C + k0, wv);
+  #pragma unroll
+          for (int q = 0; q < 8; ++q) acc += v[i][q] * wv[q];
+        }
+      }
+      e16[o] = wave_sum(acc);
+    }
+  };
+  noise(r, eps);
+  if (r_u >= 0) {
+    float eu[16];
+    noise(r_u, eu);
+#pragma unroll
+    for (int o = 0; o < 16; ++o) eps[o] = eu[o] + a.gscale * (eps[o] - eu[o]);
   }
   if (lane < 16) {
     const int o = lane, pix = o >> 2, c = o & 3, pi = pix >> 1, qi = pix & 1;
@@ -328,6 +346,11 @@ __global__ __launch_bounds__(256) void final_ddim_kernel(FinalArgs a) {
     const float xn = a.ca * a.latent_in[li] + a.cb * e;
     a.latent_out[li] = xn;
     if (a.traj_next) a.traj_next[b * a.traj_chain_stride + (li - (size_t)b * 4 * Hl * Wl)] = xn;
+    if (r_u >= 0) {  // the unconditional chain of the pair gets the same update
+      const size_t lu = li + (size_t)4 * Hl * Wl;
+      a.latent_out[lu] = xn;
+      if (a.traj_next) a.traj_next[(b + 1) * a.traj_chain_stride + (li - (size_t)b * 4 * Hl * Wl)] = xn;
+    }
   }
 }
 

@@ -169,7 +169,8 @@ class RegionCacheModel:
         abi.rc_prepare_text(self.ctx, _ptr(txt), B, _ptr(tkv), _ptr(ws), ws.numel(), _stream())
         return tkv
 
-    def _io(self, inp, timestep, timestep_next, tkv, delta, maps, latent_out, t_vec, text_valid=None):
+    def _io(self, inp, timestep, timestep_next, tkv, delta, maps, latent_out, t_vec, text_valid=None,
+            guidance=None):
         d = None
         n_delta = 0
         if delta is not None and len(delta):
@@ -180,20 +181,27 @@ class RegionCacheModel:
                             None if d is None else C.cast(d, C.POINTER(C.c_int32)), n_delta,
                             None if maps is None else maps.data_ptr(),
                             None if latent_out is None else latent_out.data_ptr(),
-                            None if text_valid is None else text_valid.data_ptr())
+                            None if text_valid is None else text_valid.data_ptr(),
+                            0 if guidance is None else 1, 0.0 if guidance is None else float(guidance))
         return io, d
 
     def build_cache(self, cache: CacheBuffer, step: int, inp: torch.Tensor, timestep: int, timestep_next: int,
-                    tkv: torch.Tensor, delta=None, maps=None, latent_out=None, t_vec=None, text_valid=None):
-        """text_valid: optional device int32 [batch] of unpadded prompt lengths."""
-        io, keep = self._io(inp, timestep, timestep_next, tkv, delta, maps, latent_out, t_vec, text_valid)
+                    tkv: torch.Tensor, delta=None, maps=None, latent_out=None, t_vec=None, text_valid=None,
+                    guidance=None):
+        """text_valid: optional device int32 [batch] of unpadded prompt lengths.
+        guidance: classifier-free guidance scale; chains 2p and 2p+1 are then
+        the conditional and unconditional branch of one image."""
+        io, keep = self._io(inp, timestep, timestep_next, tkv, delta, maps, latent_out, t_vec, text_valid,
+                            guidance)
         ws = self.workspace(cache.batch * self.N, cache.batch)
         abi.rc_build_cache(self.ctx, C.byref(cache.view), step, C.byref(io), _ptr(ws), ws.numel(), _stream())
 
     def reuse_step(self, cache: CacheBuffer, step: int, act: ActiveSet, inp: torch.Tensor, timestep: int,
                    timestep_next: int, tkv: torch.Tensor, delta=None, maps=None, latent_out=None, t_vec=None,
-                   fuse: bool = True, active_hidden: Optional[torch.Tensor] = None, text_valid=None):
-        io, keep = self._io(inp, timestep, timestep_next, tkv, delta, maps, latent_out, t_vec, text_valid)
+                   fuse: bool = True, active_hidden: Optional[torch.Tensor] = None, text_valid=None,
+                   guidance=None):
+        io, keep = self._io(inp, timestep, timestep_next, tkv, delta, maps, latent_out, t_vec, text_valid,
+                            guidance)
         ws = self.workspace(max(act.total, 1), cache.batch)
         s = act.struct()
         abi.rc_reuse_step(self.ctx, C.byref(cache.view), step, C.byref(s), C.byref(io), _ptr(active_hidden),

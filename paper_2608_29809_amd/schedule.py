@@ -25,7 +25,7 @@ from typing import List, Optional, Sequence
 import numpy as np
 import torch
 
-from .runtime import ActiveSet, CacheBuffer, RegionCacheModel
+from .runtime import ActiveSet, CacheBuffer, RegionCacheModel, compact_mask
 
 __all__ = ["timestep_grid", "prompt_similarity", "reuse_cutoff", "step_plan", "EditSession"]
 
@@ -70,9 +70,16 @@ class EditSession:
     pool equal to the latest turn's trajectory."""
 
     def __init__(self, model: RegionCacheModel, batch: int, T: int = 20, rho: float = 0.2, tau_s: float = 0.8,
-                 reading: str = "dense_then_reuse", threshold: float = 0.3, radius: int = 1):
+                 reading: str = "dense_then_reuse", threshold: float = 0.3, radius: int = 1,
+                 guidance: Optional[float] = None):
+        """guidance: classifier-free guidance scale; the batch then holds
+        (conditional, unconditional) chain pairs and the localised region of
+        each conditional chain is used for its pair."""
         if reading not in ("dense_then_reuse", "paper"):
             raise ValueError(f"unknown reading {reading!r}")
+        if guidance is not None and batch % 2:
+            raise ValueError("guidance needs (conditional, unconditional) chain pairs")
+        self.guidance = guidance
         self.model, self.batch, self.T = model, batch, T
         self.rho, self.tau_s, self.reading = rho, tau_s, reading
         self.threshold, self.radius = threshold, radius
@@ -91,7 +98,8 @@ class EditSession:
         x = x_T.contiguous()
         for s in range(self.T):
             nxt = torch.empty_like(x)
-            m.build_cache(self.cache, s, x, int(self.tgrid[s]), self._t_next(s), tkv, latent_out=nxt)
+            m.build_cache(self.cache, s, x, int(self.tgrid[s]), self._t_next(s), tkv, latent_out=nxt,
+                          guidance=self.guidance)
             x = nxt
         self.turns = 1
         return x
@@ -121,13 +129,17 @@ class EditSession:
             if what == "dense":
                 emit = region is None and s == n_dense - 1
                 maps = torch.zeros((self.batch, m.N, len(delta_cols)), device=x.device) if emit else None
-                m.build_cache(self.cache, s, x, t, tn, tkv, list(delta_cols) if emit else None, maps, nxt)
+                m.build_cache(self.cache, s, x, t, tn, tkv, list(delta_cols) if emit else None, maps, nxt,
+                              guidance=self.guidance)
                 if emit:
                     mask, act = m.localize(maps, len(delta_cols), self.threshold, self.radius)
+                    if self.guidance is not None:  # the conditional branch's region for both branches
+                        mask = mask[0::2].repeat_interleave(2, dim=0).contiguous()
+                        act = compact_mask(mask)
             elif what == "copy":
-                m.reuse_step(self.cache, s, empty, x, t, tn, tkv, latent_out=nxt)
+                m.reuse_step(self.cache, s, empty, x, t, tn, tkv, latent_out=nxt, guidance=self.guidance)
             else:
-                m.reuse_step(self.cache, s, act, x, t, tn, tkv, latent_out=nxt)
+                m.reuse_step(self.cache, s, act, x, t, tn, tkv, latent_out=nxt, guidance=self.guidance)
             x = nxt
         self.turns += 1
         return dict(latent=x, plan=plan, active=act, mask=mask)

@@ -106,7 +106,7 @@ def test_buffer_sizes(ctx):
 
 def _io(**over):
     d = dict(input=FAKE, t_vec=None, timestep=500, timestep_next=450, text_kv=FAKE, delta_cols_host=None,
-             n_delta=0, maps=None, latent_out=FAKE, text_valid=None)
+             n_delta=0, maps=None, latent_out=FAKE, text_valid=None, guided=0, guidance_scale=0.0)
     d.update(over)
     return abi.rc_step_io(*[d[f] for f, _ in abi.rc_step_io._fields_])
 
@@ -153,6 +153,25 @@ def test_reuse_validation(ctx):
     assert step(ctx, C.byref(view), 1, C.byref(a), C.byref(_io()), None, 4, FAKE, ws, None) == -1  # flags
     if NO_GPU:
         assert step(ctx, C.byref(view), 1, C.byref(a), C.byref(_io()), None, 1, FAKE, ws, None) == -6
+
+
+def test_guidance_validation(ctx):
+    """Guided steps pair chains 2p / 2p+1: odd batches and unequal pair counts
+    are refused before any launch."""
+    view1 = abi.rc_cache_view(FAKE, abi.rc_cache_bytes(ctx, 1, 4), 1, 4)
+    view2 = abi.rc_cache_view(FAKE, abi.rc_cache_bytes(ctx, 2, 4), 2, 4)
+    ws = abi.rc_workspace_bytes(ctx, 2048, 2)
+    build, step = abi.LIB.rc_build_cache, abi.LIB.rc_reuse_step
+    g = _io(guided=1, guidance_scale=4.5)
+    assert build(ctx, C.byref(view1), 0, C.byref(g), FAKE, ws, None) == -2           # odd batch
+    assert build(ctx, C.byref(view2), 0, C.byref(_io(guided=2)), FAKE, ws, None) == -1
+    assert build(ctx, C.byref(view2), 0, C.byref(_io(guided=1, guidance_scale=float("nan"))), FAKE, ws,
+                 None) == -1
+    h = (C.c_int32 * 3)(0, 10, 19)
+    a = abi.rc_active_set(FAKE, FAKE, C.cast(h, C.POINTER(C.c_int32)), 2)
+    assert step(ctx, C.byref(view2), 1, C.byref(a), C.byref(g), None, 1, FAKE, ws, None) == -4  # 10 vs 9
+    if NO_GPU:
+        assert build(ctx, C.byref(view2), 0, C.byref(g), FAKE, ws, None) == -6
 
 
 def test_localize_and_logits_validation(ctx):

@@ -540,3 +540,25 @@ def test_final_layer_matches_torch():
     h = ln(torch.from_numpy(X)) * (1 + sc) + sh
     ref = _linear(W["fin_w"], W["fin_b"])(h).detach().numpy()
     assert _rel(O.final_layer(W, X, temb), ref) < 1e-13
+
+
+def test_guided_latent_special_cases():
+    """Classifier-free guidance: scale 1 is the conditional step and scale 0
+    the unconditional step (each the oracle's own unguided reuse step);
+    the guided noise is affine in the scale."""
+    s = TINY
+    W, lat, tkv_c, cache, lnc, rng = _tiny_step_inputs(31)
+    y_u = O.caption_projection(W, np.zeros((s.text_len, s.text_dim)))
+    tkv_u = [O.text_kv(lw, y_u, s.heads) for lw in W["layers"]]
+    idx = np.flatnonzero(rng.random(s.tokens) < 0.4)
+    rc = O.reuse_step(s, W, lat, 500, 450, tkv_c, idx, cache, lnc)
+    ru = O.reuse_step(s, W, lat, 500, 450, tkv_u, idx, cache, lnc)
+    g1 = O.guided_latent(s, lat, lnc, idx, rc["eps"], ru["eps"], 1.0, 500, 450)
+    g0 = O.guided_latent(s, lat, lnc, idx, rc["eps"], ru["eps"], 0.0, 500, 450)
+    assert _rel(g1, rc["latent_next"]) < 1e-12 and _rel(g0, ru["latent_next"]) < 1e-12
+    e2 = O.guided_noise(rc["eps"], ru["eps"], 2.0)
+    assert _rel(e2, 2.0 * rc["eps"] - ru["eps"]) < 1e-12
+    # the dense step's noise prediction plugs in the same way
+    dc = O.dense_step(s, W, lat, 500, 450, tkv_c)
+    assert _rel(O.guided_latent(s, lat, lnc, np.arange(s.tokens), dc["eps"], dc["eps"], 4.5, 500, 450),
+                dc["latent_next"]) < 1e-12

@@ -437,3 +437,62 @@ def test_padded_prompts_per_chain():
         assert relerr(got["H"][:, b], ref["H"]) < 2e-2
         assert relerr(to_np(out2)[b], ref["latent_next"]) < 2e-2
 
+
+@pytest.mark.gpu
+@pytest.mark.timeout(300)
+def test_guided_pair_reuse_and_dense():
+    """Classifier-free guidance: chains 0/1 are the conditional and null-prompt
+    branches of one image (own caches, same latent, same region).  Both get
+    the DDIM update of eps_u + 4.5 (eps_c - eps_u); each branch's cache
+    matches its own unguided oracle step."""
+    _say("guided pair")
+    s = synth.ModelShape(layers=2, grid_h=32, grid_w=32, dtype="bf16")
+    W = weights(s, 9, True)
+    g = 4.5
+    txt = synth.make_text(s, 2, 9)
+    txt[1] = 0.0  # null prompt features
+    lat1 = synth.make_latent(s, 1, 9)
+    lat = np.concatenate([lat1, lat1])
+    lnc1 = synth.make_latent(s, 1, 9, stream=77)
+    lnc = np.concatenate([lnc1, lnc1])
+    slot = synth.make_cache_slot(s, 2, 9)
+    model = RegionCacheModel(s, W)
+    cache = model.alloc_cache(2, 2)
+    upload_slot(model, cache, 1, slot)
+    for b in range(2):
+        cache.latent(b, 2).copy_(torch.from_numpy(lnc[b]))
+    tkv = model.prepare_text(model.to_storage(txt))
+    idx = np.sort(np.random.default_rng(9).choice(s.tokens, 200, replace=False))
+    act = ActiveSet.from_lists([idx, idx])
+    out = torch.empty(lat.shape, device="cuda")
+    model.reuse_step(cache, 1, act, torch.from_numpy(lat).cuda(), 500, 450, tkv, latent_out=out, guidance=g)
+    torch.cuda.synchronize()
+    got = download_slot(cache, 1, s.layers, 2)
+    o = to_np(out)
+    assert np.array_equal(o[0], o[1])
+    assert np.array_equal(to_np(cache.latent(0, 2)), to_np(cache.latent(1, 2)))
+    refs = []
+    for b in range(2):
+        cs = dict(K=slot["K"][:, b], V=slot["V"][:, b], H=slot["H"][:, b])
+        refs.append(O.reuse_step(s, W, lat[b], 500, 450, oracle_text_kv(s, W, txt[b]), idx, cs, lnc[b]))
+        for k in ("H", "K", "V"):
+            e = relerr(got[k][:, b][:, idx] if k == "H" else got[k][:, b][:, :, idx],
+                       refs[b][k][:, idx] if k == "H" else refs[b][k][:, :, idx])
+            assert e < 2e-2, (b, k, e)
+    ref_lat = O.guided_latent(s, lat1[0], lnc1[0], idx, refs[0]["eps"], refs[1]["eps"], g, 500, 450)
+    e = relerr(o[0], ref_lat)
+    _say("guided latent", e)
+    assert e < 2e-2
+    # the unguided result differs: guidance is applied
+    assert relerr(o[0], refs[0]["latent_next"]) > 1e-3
+    # dense step of the pair
+    out2 = torch.empty_like(out)
+    model.build_cache(cache, 0, torch.from_numpy(lat).cuda(), 700, 650, tkv, latent_out=out2, guidance=g)
+    torch.cuda.synchronize()
+    dc = O.dense_step(s, W, lat1[0], 700, 650, oracle_text_kv(s, W, txt[0]))
+    du = O.dense_step(s, W, lat1[0], 700, 650, oracle_text_kv(s, W, txt[1]))
+    ref2 = O.guided_latent(s, lat1[0], lat1[0], np.arange(s.tokens), dc["eps"], du["eps"], g, 700, 650)
+    o2 = to_np(out2)
+    assert np.array_equal(o2[0], o2[1])
+    assert relerr(o2[0], ref2) < 2e-2
+

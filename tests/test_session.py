@@ -132,3 +132,26 @@ def test_paper_plan_copy_and_region_reuse():
         assert not np.array_equal(x1[b][:, ~pix], to_np(x0)[b][:, ~pix])
     with pytest.raises(ValueError):
         sess.edit_turn(model.to_storage(txt1), xT, delta, similarity=0.2)
+
+
+@pytest.mark.gpu
+@pytest.mark.timeout(300)
+def test_guided_session_pairs_stay_in_step():
+    """With guidance the two branches of an image share latents and region:
+    both chains of each pair end every turn with identical latents, and the
+    localised region of the conditional branch is used for both."""
+    s, W, model, txt0, txt1, delta, x_T = _setup(seed=13, B=2)
+    txt0[1] = 0.0
+    txt1[1] = 0.0
+    x_T[1] = x_T[0]
+    sess = S.EditSession(model, 2, T=5, guidance=4.5)
+    xT = torch.from_numpy(x_T).cuda()
+    x0 = sess.first_turn(model.to_storage(txt0), xT)
+    out = sess.edit_turn(model.to_storage(txt1), xT, delta)
+    torch.cuda.synchronize()
+    assert torch.equal(x0[0], x0[1])
+    assert torch.equal(out["latent"][0], out["latent"][1])
+    m = to_np(out["mask"])
+    assert np.array_equal(m[0], m[1])
+    assert out["active"].counts[0] == out["active"].counts[1] == int(m[0].sum())
+
