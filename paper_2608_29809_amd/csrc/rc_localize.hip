@@ -8,73 +8,89 @@
 
 namespace rc {
 
-constexpr int LG_ROWS = 256;  // logits rows (tokens) per workgroup
+constexpr int LG_TOK = 64;  // tokens per workgroup, 16 per wave
 
-// partial[l][tok][j] = sum_h softmax(Z[l][h][tok][:])[delta_j]; one workgroup
-// per (256-token tile, layer); each head's 256 rows are one contiguous block
-// of the logits, staged through LDS with 16-byte coalesced loads, then each
-// thread reduces its own row.
+// partial[l][tok][j] = sum_h softmax(Z[l][h][tok][:])[delta_j].  One
+// workgroup per (64-token tile, layer), each wave 16 tokens.  A row of the
+// logits (text_len <= 128 bf16, 16-byte chunks) is spread over one 16-lane
+// group, so a load instruction covers four consecutive rows -- contiguous
+// memory -- and the row's max and sum are 16-lane reductions.  Lane j of a
+// group owns delta column j: it re-reads that one logit (a cache hit) and
+// accumulates its probability.  The next head's rows are loaded while the
+// current head is reduced.
 __global__ __launch_bounds__(256) void maps_from_logits_kernel(const uint16_t *Z, int heads, int tokens,
                                                                int text_len, MapsDelta dl, float *partial) {
-  extern __shared__ __attribute__((aligned(16))) uint16_t rowbuf[];
-  const int l = blockIdx.y, tok0 = blockIdx.x * LG_ROWS, tid = threadIdx.x;
-  const int nrows = min(LG_ROWS, tokens - tok0);
-  const int row_vec = text_len / 8;                       // 16-byte vectors per row
-  const int ld = (row_vec & 1) ? text_len : text_len + 8; // odd count of 16-byte slots per row
-  float acc[8];
+  const int l = blockIdx.y, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int grp = lane >> 4, j16 = lane & 15;
+  const int tok_w = blockIdx.x * LG_TOK + wave * 16;  // first token of this wave
+  const int row_vec = text_len / 8;                    // 16-byte chunks per row
+  const bool lane_on = j16 < row_vec;
+  const bool owner = j16 < dl.n;
+  int my_col = 0;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) acc[j] = 0.0f;
-  for (int h = 0; h < heads; ++h) {
-    const uint16_t *src = Z + (((size_t)l * heads + h) * tokens + tok0) * text_len;
-    const int nvec = nrows * row_vec;
-    __syncthreads();
-    for (int v = tid; v < nvec; v += 256) {
-      const int r = v / row_vec, c = v - r * row_vec;
-      *(V16 *)(rowbuf + r * ld + c * 8) = *(const V16 *)(src + (size_t)v * 8);
+  for (int j = 0; j < 8; ++j)
+    if (j == j16) my_col = dl.col[j];
+  constexpr float kLog2e = 1.4426950408889634f;
+  auto load = [&](int h, V16 *v, uint16_t *zd) {
+    const uint16_t *blk = Z + ((size_t)(l * heads + h) * tokens + tok_w) * text_len;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = i * 4 + grp;
+      const bool ok = tok_w + row < tokens;
+      v[i] = V16{{0u, 0u, 0u, 0u}};
+      if (lane_on && ok) v[i] = *(const V16 *)(blk + (size_t)row * text_len + j16 * 8);
+      zd[i] = (owner && ok) ? blk[(size_t)row * text_len + my_col] : (uint16_t)0;
     }
-    __syncthreads();
-    if (tid < nrows) {
-      const uint16_t *row = rowbuf + tid * ld;
-      uint32_t w[64];
+  };
+  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  V16 cur[4], nxt[4];
+  uint16_t zc[4], zn[4];
+  load(0, cur, zc);
+  for (int h = 0; h < heads; ++h) {
+    if (h + 1 < heads) load(h + 1, nxt, zn);
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        V16 t = V16{{0u, 0u, 0u, 0u}};
-        if (v < row_vec) t = *(const V16 *)(row + v * 8);
+    for (int i = 0; i < 4; ++i) {
+      float z[8];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) w[v * 4 + q] = t.w[q];
+      for (int q = 0; q < 4; ++q) {
+        z[2 * q] = __uint_as_float(cur[i].w[q] << 16);
+        z[2 * q + 1] = __uint_as_float(cur[i].w[q] & 0xFFFF0000u);
       }
       float m = -INFINITY;
+      if (lane_on)
+        m = fmaxf(fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3])), fmaxf(fmaxf(z[4], z[5]), fmaxf(z[6], z[7])));
 #pragma unroll
-      for (int k = 0; k < 128; ++k) {
-        const float z = __uint_as_float((k & 1) ? (w[k >> 1] & 0xFFFF0000u) : (w[k >> 1] << 16));
-        if (k < text_len) m = fmaxf(m, z);
-      }
-      float s = 0.0f;
+      for (int o = 8; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 16));
+      const float mc = m * kLog2e;
+      float sum = 0.0f;
+      if (lane_on)
 #pragma unroll
-      for (int k = 0; k < 128; ++k) {
-        const float z = __uint_as_float((k & 1) ? (w[k >> 1] & 0xFFFF0000u) : (w[k >> 1] << 16));
-        if (k < text_len) s += __expf(z - m);
-      }
-      const float inv = 1.0f / s;
+        for (int q = 0; q < 8; ++q) sum += exp2f(__builtin_fmaf(z[q], kLog2e, -mc));
 #pragma unroll
-      for (int j = 0; j < 8; ++j)
-        if (j < dl.n) acc[j] += __expf(__uint_as_float((uint32_t)row[dl.col[j]] << 16) - m) * inv;
+      for (int o = 8; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 16);
+      if (owner) acc[i] += exp2f(__builtin_fmaf(__uint_as_float((uint32_t)zc[i] << 16), kLog2e, -mc)) / sum;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      cur[i] = nxt[i];
+      zc[i] = zn[i];
     }
   }
-  if (tid < nrows) {
-    for (int j = 0; j < dl.n; ++j) partial[((size_t)l * tokens + tok0 + tid) * dl.n + j] = acc[j];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int tok = tok_w + i * 4 + grp;
+    if (owner && tok < tokens) partial[((size_t)l * tokens + tok) * dl.n + j16] = acc[i];
   }
 }
 
 hipError_t launch_maps_from_logits(const uint16_t *logits, int n_layers, int heads, int tokens, int text_len,
                                    const int *delta, int n_delta, float *partial, hipStream_t s) {
+  if (text_len % 8 || text_len > 128 || n_delta < 1 || n_delta > 8) return hipErrorInvalidValue;
   MapsDelta dl;
   dl.n = n_delta;
   for (int j = 0; j < 8; ++j) dl.col[j] = j < n_delta ? delta[j] : 0;
-  dim3 grid((tokens + LG_ROWS - 1) / LG_ROWS, n_layers);
-  const int ld = ((text_len / 8) & 1) ? text_len : text_len + 8;
-  const size_t lds = (size_t)LG_ROWS * ld * sizeof(uint16_t);
-  rc_launch(maps_from_logits_kernel, grid, dim3(256), lds, s, logits, heads, tokens, text_len, dl, partial);
+  dim3 grid((tokens + LG_TOK - 1) / LG_TOK, n_layers);
+  rc_launch(maps_from_logits_kernel, grid, dim3(256), 0, s, logits, heads, tokens, text_len, dl, partial);
   return hipGetLastError();
 }
 
