@@ -425,7 +425,7 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
         a.pmaps = pmaps;
       }
       RC_TRY(timed(c, RC_KC_ATTN_CROSS, s, [&] {
-        return sizeof(T) == 2 ? rc::launch_attention2(a, B, max_rb, true, s)
+        return sizeof(T) == 2 ? rc::launch_attention2(a, B, max_rb, s)
                               : rc::launch_attention<T>(a, B, max_rb, emit, s);
       }));
       if (emit)

@@ -1,4 +1,7 @@
-// bf16 variable-query-length attention, second form (head dim 72).
+// bf16 cross-attention of the active rows to the text tokens (head dim 72),
+// with the delta-column probabilities of the localisation maps (Sec. 3.2).
+// The text values are stored transposed ([72][keys] per head).  (The self-
+// attention over the cache, rc_attn3.hip, descends from this kernel.)
 //
 // Same decomposition as rc_attn.hip -- one workgroup = 4 waves = 128 queries
 // of one (chain, head, key range), each wave 32 queries, scores formed
@@ -27,9 +30,6 @@
 namespace rc {
 
 constexpr int A2_BQ = 128, A2_BK = 64;
-#ifndef ATT2_STAGES
-#define ATT2_STAGES 2
-#endif
 
 __device__ __forceinline__ int key_perm2(int m) {
   return ((m >> 4) & 1) * 16 + ((m >> 2) & 1) * 8 + ((m >> 3) & 1) * 4 + (m & 3);
@@ -287,14 +287,11 @@ __global__ __launch_bounds__(256, 2) void attn2_kernel(AttnArgs a) {
   }
 }
 
-hipError_t launch_attention2(const AttnArgs &a, int n_chains, int max_rows, bool cross, hipStream_t s) {
+hipError_t launch_attention2(const AttnArgs &a, int n_chains, int max_rows, hipStream_t s) {
   if (max_rows <= 0) return hipSuccess;
   if (a.n_keys % A2_BK != 0 || a.splits < 1 || a.splits > a.n_keys / A2_BK || a.v_rowmajor) return hipErrorInvalidValue;
   dim3 grid((max_rows + A2_BQ - 1) / A2_BQ, (a.hidden / kHeadDim) * a.splits, n_chains);
-  if (cross)
-    rc_launch(attn2_kernel<true, 2>, grid, dim3(256), 0, s, a);
-  else
-    rc_launch(attn2_kernel<false, ATT2_STAGES>, grid, dim3(256), 0, s, a);
+  rc_launch(attn2_kernel<true, 2>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -106,6 +106,7 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
     }
   }
 
+  const f32x16 zero16 = {};  // C operand of a tile's first score MFMA, kept live
   // S^T of one tile: lane group g, sub-tile st, accumulator e = c*8 + k  <->
   // key st*32 + c*16 + g*8 + k
   auto scores = [&](int stage, f32x16 *s) {
@@ -123,7 +124,7 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
     for (int c = 0; c < 5; ++c)
 #pragma unroll
       for (int st = 0; st < 2; ++st)
-        s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st][c], qf[c], c == 0 ? f32x16{} : s[st], 0, 0, 0);
+        s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st][c], qf[c], c == 0 ? zero16 : s[st], 0, 0, 0);
   };
 
   f32x16 o[3];
@@ -173,7 +174,9 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
   // One key tile: wait for tile+1 and recycle the slot of tile-1, update the
   // running maximum, then (one basic block) the score MFMAs of tile+1
   // interleaved with the exponentials of tile, then the PV MFMAs of tile.
-  auto step = [&](int tile, auto has_next_c) {
+  // the scores of the current tile arrive in s_cur; those of the next tile
+  // are formed in s_nxt (the caller alternates the two buffers)
+  auto step = [&](int tile, auto has_next_c, f32x16 *s_cur, f32x16 *s_nxt) {
     constexpr bool HAS_NEXT = decltype(has_next_c)::value;
     const int stage = (tile - t_beg) % A3_STAGES;
     // tile+1 has landed (the only loads in flight) and every wave is done with
@@ -212,13 +215,12 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
     }
     const float mc = (m_run == -INFINITY) ? 0.0f : m_run * c2;
 
-    f32x16 s_next[2];
     if (HAS_NEXT) {
 #pragma unroll
       for (int c = 0; c < 5; ++c)
 #pragma unroll
         for (int st = 0; st < 2; ++st)
-          s_next[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st][c], qf[c], c == 0 ? f32x16{} : s_next[st], 0, 0, 0);
+          s_nxt[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st][c], qf[c], c == 0 ? zero16 : s_nxt[st], 0, 0, 0);
     }
     bf16x8 pf[2][2];
 #pragma unroll
@@ -247,13 +249,19 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
         for (int t = 0; t < 3; ++t)
           o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(vs, kb, t), pf[st][c], o[t], 0, 0, 0);
       }
-    if (HAS_NEXT) {
-      s_cur[0] = s_next[0];
-      s_cur[1] = s_next[1];
-    }
   };
-  for (int tile = t_beg; tile + 1 < t_end; ++tile) step(tile, std::true_type{});
-  step(t_end - 1, std::false_type{});
+  f32x16 s_alt[2];
+  int tile = t_beg;
+  for (; tile + 2 < t_end; tile += 2) {
+    step(tile, std::true_type{}, s_cur, s_alt);
+    step(tile + 1, std::true_type{}, s_alt, s_cur);
+  }
+  if (tile + 1 < t_end) {
+    step(tile, std::true_type{}, s_cur, s_alt);
+    step(tile + 1, std::false_type{}, s_alt, s_cur);
+  } else {
+    step(tile, std::false_type{}, s_cur, s_alt);
+  }
 
   const float l_tot = __shfl(o[2][4], r32, 64);  // output row 72: the denominator
   if (!q_ok) return;

@@ -92,8 +92,9 @@ hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &plan, float 
                         const LnNext *ln = nullptr, bool *ln_done = nullptr);
 template <typename T> hipError_t launch_attention(const AttnArgs &a, int n_chains, int max_rows,
                                                   bool emit_maps, hipStream_t s);
-// bf16 attention with direct-to-LDS tiles and uneven key splits (rc_attn2.hip).
-hipError_t launch_attention2(const AttnArgs &a, int n_chains, int max_rows, bool cross, hipStream_t s);
+// bf16 cross-attention to the transposed text values, emitting the
+// delta-column maps when a.pmaps is set (rc_attn2.hip).
+hipError_t launch_attention2(const AttnArgs &a, int n_chains, int max_rows, hipStream_t s);
 // bf16 self-attention with the next tile's score MFMAs overlapping the
 // softmax (rc_attn3.hip); no map emission.
 hipError_t launch_attention3(const AttnArgs &a, int n_chains, int max_rows, hipStream_t s);
