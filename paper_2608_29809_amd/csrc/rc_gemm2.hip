@@ -315,16 +315,56 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
         *(f32x4 *)(P + (size_t)m * g.N + n0 + c4) = v;
       }
     } else if (!transposed) {
-      for (int idx = tid; idx < HB * BN / 4; idx += NT) {
-        const int row = idx / (BN / 4), c4 = (idx % (BN / 4)) * 4;
+      // a thread keeps one group of 4 columns over the band's rows: column
+      // data is loaded once, and every row-dependent load (residual, packed
+      // row id) is issued before the first store so their latencies overlap
+      static_assert(NT % (BN / 4) == 0, "a thread keeps its columns over the band");
+      constexpr int RPI = NT / (BN / 4), IT = (HB + RPI - 1) / RPI;
+      const int c4 = (tid % (BN / 4)) * 4, row0 = tid / (BN / 4);
+      const int n = n0 + c4;
+      const f32x4 bb = g.bias ? *(const f32x4 *)(g.bias + n) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+      constexpr bool NEED_X = EPI == EPI_RESID;
+      const bool need_rows = (EPI == EPI_RESID && g.hslot) || (EPI == EPI_QKV && tile_part > 0);
+      f32x4 gt = f32x4{1.0f, 1.0f, 1.0f, 1.0f};
+      if (EPI == EPI_RESID && g.gate) {
+        gt = *(const f32x4 *)(g.gate + n);
+        if (g.gate2) gt += *(const f32x4 *)(g.gate2 + n);
+      }
+      f32x4 xo[NEED_X ? IT : 1];
+      int pk[IT];
+#pragma unroll
+      for (int it = 0; it < IT; ++it) {
+        const int m = min(m0 + rb + min(row0 + it * RPI, HB - 1), g.M - 1);
+        if (NEED_X) xo[it] = *(const f32x4 *)(g.X + (size_t)m * g.ldx + n);
+        pk[it] = need_rows ? g.rows[m] : 0;
+      }
+#pragma unroll
+      for (int it = 0; it < IT; ++it) {
+        const int row = row0 + it * RPI;
         const int m = m0 + rb + row;
-        if (m >= g.M) continue;
-        const int n = n0 + c4;
-        const f32x4 bb = g.bias ? *(const f32x4 *)(g.bias + n) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        if ((IT * RPI != HB && row >= HB) || m >= g.M) continue;
         float v[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) v[q] = tile_at(row, c4 + q) + bb[q];
-        epi4<EPI>(g, m, n, v, tile_part);
+        if (EPI == EPI_RESID) {
+          f32x4 x;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            x[q] = xo[NEED_X ? it : 0][q] + gt[q] * v[q];
+            v[q] = x[q];
+          }
+          *(f32x4 *)(g.X + (size_t)m * g.ldx + n) = x;
+          if (g.xt) st4((bf16 *)g.xt + (size_t)m * g.ldx + n, v);
+          if (g.hrows) st4((bf16 *)g.hrows + (size_t)m * g.N + n, v);
+          if (g.hslot)
+            st4((bf16 *)g.hslot + row_chain(pk[it]) * g.chain_stride + (size_t)row_token(pk[it]) * g.hidden + n, v);
+        } else if (EPI == EPI_QKV && tile_part > 0) {
+          const int c = n - tile_part * g.hidden, hh = c / kHeadDim, dd = c - hh * kHeadDim;
+          st4((bf16 *)(tile_part == 1 ? g.kslot : g.vslot) + (size_t)row_chain(pk[it]) * g.chain_stride +
+                  ((size_t)hh * g.tokens + row_token(pk[it])) * kHeadDim + dd, v);
+        } else {
+          epi4<EPI>(g, m, n, v, tile_part);
+        }
       }
     } else {
       // a wave walks one column, lanes on consecutive rows: each store covers
