@@ -7,8 +7,8 @@
 //   (lane l reads row l%32, chunk 2kk + l/32) hit distinct LDS banks.
 // * STAGES-deep ring of LDS buffers, one barrier per 64-wide K step; loads
 //   for step k+STAGES-1 are issued right after the barrier of step k.
-// * 256 threads = 4 waves in a 2x2 grid, each wave a (BM/2)x(BN/2) block of
-//   32x32x16 MFMAs.
+// * A K group is 4 or 8 waves in a WGM x WGN grid, each wave a
+//   (BM/WGM)x(BN/WGN) block of 32x32x16 MFMAs.
 // * Split-K over grid.z: each split writes an fp32 partial tile and a
 //   separate kernel sums the splits in a fixed order and applies the
 //   epilogue, so results do not depend on scheduling.
@@ -508,45 +508,45 @@ static void launch_reduce(const GemmArgs &a, int epi, int splits, const float *p
 #undef RC_RD
 }
 
-// Choice of tile, K groups and split count for a shape, from sweeps on the
-// step's shapes with cold weights (412 to 16384 rows; N in {1152, 3456,
-// 4608}; K in {1152, 4608}).  A K step costs roughly the same time whatever
-// the tile, so a workgroup's time is set by its K steps: when the grid is
-// small the rows are cut into 32-row tiles and K over two groups of waves in
-// one workgroup (each CU runs one such workgroup), as long as the grid still
-// fits the 256 CUs in one wave of workgroups; large grids keep 64x128 tiles
-// with two workgroups per CU.  Split-K over the grid only pays for K = 4608
-// at few tiles.
+// Choice of tile, wave layout, K groups and split count for a shape, from
+// sweeps on the step's shapes with the activations in cache and the weights
+// cold (410 to 4096 rows; N in {1152, 3456, 4608}; K in {1152, 4608}).  The
+// operand traffic into a CU (L2 -> LDS, ~64 bytes per clock) bounds small
+// tiles, and a workgroup's time is set by its K steps: a grid that fits the
+// 256 CUs in one wave of workgroups takes the largest tile that still fills
+// them, with eight waves (32x32 or 32x64 / 64x32 per wave) where the tile
+// allows it; grids of one to two waves of 64-row tiles keep 64x128 with two
+// workgroups per CU.  Split-K over the grid pays only for K = 4608.
 GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats) {
-  GemmPlan p{64, 128, 1, 1, 2};
+  GemmPlan p{64, 128, 1, 1, 2, 2, 2};
   const int nk = K / G2_BK;
-  const long t64 = (long)((M + 63) / 64) * (N / 128), t32 = (long)((M + 31) / 32) * (N / 128);
+  const long tn = N / 128;
+  const long t32 = (long)((M + 31) / 32) * tn, t64 = (long)((M + 63) / 64) * tn, t128 = (long)((M + 127) / 128) * tn;
+  auto set = [&](int bm, int kg, int stages, int wgm, int wgn) {
+    p.bm = bm; p.kg = kg; p.stages = stages; p.wgm = wgm; p.wgn = wgn;
+  };
   if (K >= 2048) {
-    if (t64 < 384 && nk % 4 == 0 && (size_t)2 * M * N <= partial_cap_floats) {
+    const bool room = (size_t)2 * M * N <= partial_cap_floats;
+    if (t64 < 160 && nk % 4 == 0 && room) {
       p.splits = 2;
-      p.kg = 2;
-      p.stages = 3;
-      if (t32 * 2 <= 256) p.bm = 32;
-    } else if (t64 < 160 && nk % 2 == 0) {
-      p.kg = 2;
-      p.stages = 3;
+      if (t32 * 2 <= 256) set(32, 2, 3, 1, 4);
+      else set(64, 2, 3, 2, 2);
+    } else if (t64 < 384 && nk % 2 == 0 && room) {
+      p.splits = 2;
+      set(64, 1, 3, 2, 4);
     }
     return p;
   }
-  if (N >= 3072 && M >= 1536 && M <= 8192) {
-    p.bm = 128;  // wide outputs at a few thousand rows: 64x64 waves, two workgroups per CU
+  if (N >= 3072) {
+    if (t64 <= 256) set(64, 1, 3, 2, 4);
+    else if (t128 <= 256) set(128, 1, 3, N % 512 ? 4 : 2, N % 512 ? 2 : 4);
+    else if (M < 3072) set(128, 1, 2, 4, 2);
+    else set(128, 1, 2, 2, 2);
     return p;
   }
-  if (nk % 2 == 0) {
-    if (t32 <= 256) {
-      p.bm = 32;
-      p.kg = 2;
-      p.stages = 3;
-    } else if (t64 <= 256) {
-      p.kg = 2;
-      p.stages = 3;
-    }
-  }
+  if (nk % 2 == 0 && t32 <= 256) set(32, 2, 3, 1, 4);
+  else if (nk % 2 == 0 && t64 <= 256) set(64, 2, 3, 2, 2);
+  else if (t64 <= 512) set(64, 1, 3, 2, 4);
   return p;
 }
 
@@ -556,21 +556,26 @@ hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &pl, float *p
   if (a.M <= 0) return hipSuccess;
   if (pl.bn != 128 || a.N % 128 || a.K % (G2_BK * pl.splits * pl.kg)) return hipErrorInvalidValue;
   const bool split = pl.splits > 1;
-  // tile shapes: 128 rows = 2x2 waves of 64x64; 64 rows = 2x2 waves of 32x64;
-  // 32 rows = 1x4 waves of 32x32
+  // 4-wave K groups: 128 rows = 2x2 waves of 64x64, 64 rows = 2x2 of 32x64,
+  // 32 rows = 1x4 of 32x32; 8-wave: 128 rows = 4x2 of 32x64 or 2x4 of 64x32,
+  // 64 rows = 2x4 of 32x32
 #define RC_G2(BMV, KGV, STG, WM_, WN_)                                                       \
   {                                                                                          \
     if (split) launch_g2<BMV, 128, STG, KGV, WM_, WN_, true>(a, epi, pl.splits, partial, s); \
     else launch_g2<BMV, 128, STG, KGV, WM_, WN_, false>(a, epi, 1, nullptr, s);              \
   }
-  const int cfg = pl.bm * 100 + pl.kg * 10 + pl.stages;
+  const int cfg = pl.bm * 10000 + pl.kg * 1000 + pl.stages * 100 + pl.wgm * 10 + pl.wgn;
   switch (cfg) {
-    case 6412: RC_G2(64, 1, 2, 2, 2) break;
-    case 6423: RC_G2(64, 2, 3, 2, 2) break;
-    case 3213: RC_G2(32, 1, 3, 1, 4) break;
-    case 3223: RC_G2(32, 2, 3, 1, 4) break;
-    case 3232: RC_G2(32, 3, 2, 1, 4) break;
-    case 12812: RC_G2(128, 1, 2, 2, 2) break;
+    case 641222: RC_G2(64, 1, 2, 2, 2) break;
+    case 642322: RC_G2(64, 2, 3, 2, 2) break;
+    case 641324: RC_G2(64, 1, 3, 2, 4) break;
+    case 321314: RC_G2(32, 1, 3, 1, 4) break;
+    case 322314: RC_G2(32, 2, 3, 1, 4) break;
+    case 323214: RC_G2(32, 3, 2, 1, 4) break;
+    case 1281222: RC_G2(128, 1, 2, 2, 2) break;
+    case 1281242: RC_G2(128, 1, 2, 4, 2) break;
+    case 1281342: RC_G2(128, 1, 3, 4, 2) break;
+    case 1281324: RC_G2(128, 1, 3, 2, 4) break;
     default: return hipErrorInvalidValue;
   }
 #undef RC_G2

@@ -71,8 +71,9 @@ template <typename T> hipError_t launch_gemm(const GemmArgs &a, int epi, hipStre
 
 // bf16 GEMM with direct-to-LDS staging and optional split-K (rc_gemm2.hip).
 struct GemmPlan {
-  int bm, bn, splits, kg;  // kg: K groups inside one workgroup (4 waves each)
+  int bm, bn, splits, kg;  // kg: K groups inside one workgroup
   int stages;              // LDS ring depth per K group
+  int wgm, wgn;            // waves of one K group along M and N (4 or 8 waves)
 };
 GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats);
 // LayerNorm + modulation of the next block applied to the rows a residual
