@@ -1,6 +1,6 @@
-// bf16 self-attention, third form: the score MFMAs of key tile t+1 are issued
-// before the softmax of tile t, so the matrix core works on S(t+1) while the
-// vector ALUs exponentiate S(t) within the same wave.
+// bf16 self-attention, third form: a software pipeline over the key tiles in
+// which the matrix core works on the scores of tile t+1 and the PV product of
+// tile t-1 while the vector ALUs exponentiate tile t, within the same wave.
 //
 // Decomposition, operand layouts and numerics are those of attn2_kernel
 // (rc_attn2.hip): 128 queries of one (chain, head, key range) per workgroup,
@@ -9,14 +9,20 @@
 // denominator; exp2 online softmax with the lazy rescale; uneven key splits
 // and the deterministic combine.  Differences:
 //
-// * a three-tile ring: while tile t's values are read and tile t+1's keys are
-//   read, tile t+2 streams in; one barrier per tile;
-// * the loop carries the scores of the next tile in registers;
+// * a four-slot ring: while tile t-1's values and tile t+1's keys are read,
+//   tile t+2 streams in; one barrier per tile;
+// * the loop carries the scores of the next tile and the probabilities of
+//   the previous tile in registers; a rescale of the reference maximum is
+//   applied after the previous tile's PV product has been added, so the
+//   accumulator sees the same operations in the same order as a
+//   tile-by-tile loop;
 // * values are stored token-major like the keys ([n_keys][72] per head), so
 //   a tile is one contiguous 9216-byte copy; the V^T operand fragments are
 //   assembled by LDS transpose reads (ds_read_b64_tr_b16: within a 16-lane
 //   group, lane i's k-th element is element i%4 of the 4-element chunk whose
-//   address lane 4k + i/4 supplied), two per fragment.
+//   address lane 4k + i/4 supplied), two per fragment;
+// * tile copies go through lds_dma16 (explicit waits), so the fragment reads
+//   of resident tiles do not wait for the copy just issued.
 #include "rc_common.h"
 #include "rc_launch.h"
 #include "rc_internal.h"
@@ -25,7 +31,7 @@
 
 namespace rc {
 
-constexpr int A3_BQ = 128, A3_BK = 64, A3_STAGES = 3;
+constexpr int A3_BQ = 128, A3_BK = 64, A3_STAGES = 4;
 
 __device__ __forceinline__ int key_perm3(int m) {
   return ((m >> 4) & 1) * 16 + ((m >> 2) & 1) * 8 + ((m >> 3) & 1) * 4 + (m & 3);
@@ -68,17 +74,13 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < 3; ++i) {
       const int base = i * 256 + wave * 64;
-      if (base < K_CH)
-        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)(kt + (base + lane) * 16),
-                                         (__attribute__((address_space(3))) void *)(ks + base * 16), 16, 0, 0);
+      if (base < K_CH) lds_dma16(kt + (base + lane) * 16, ks + base * 16);
     }
     const char *vt = (const char *)(Vg + (size_t)key0 * D);
 #pragma unroll
     for (int i = 0; i < 3; ++i) {
       const int base = i * 256 + wave * 64;
-      if (base < K_CH)
-        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)(vt + (base + lane) * 16),
-                                         (__attribute__((address_space(3))) void *)(vs + base * 16), 16, 0, 0);
+      if (base < K_CH) lds_dma16(vt + (base + lane) * 16, vs + base * 16);
     }
   };
   // the first two key tiles depend only on (chain, head, key range): they
@@ -171,22 +173,24 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
   f32x16 s_cur[2];
   scores(0, s_cur);
 
-  // One key tile: wait for tile+1 and recycle the slot of tile-1, update the
-  // running maximum, then (one basic block) the score MFMAs of tile+1
-  // interleaved with the exponentials of tile, then the PV MFMAs of tile.
-  // the scores of the current tile arrive in s_cur; those of the next tile
-  // are formed in s_nxt (the caller alternates the two buffers)
-  auto step = [&](int tile, auto has_next_c, f32x16 *s_cur, f32x16 *s_nxt) {
+  // One key tile i (tile = t_beg + i): wait for tile i+1 and recycle the slot
+  // of tile i-2 for tile i+2, update the running maximum with tile i's
+  // scores, then one interleaved block: the score MFMAs of tile i+1 and the
+  // PV MFMAs of tile i-1 (probabilities from the previous step, values still
+  // in their ring slot) run while the vector ALUs exponentiate tile i.  A
+  // rescale of the reference maximum is applied to o after the block, once
+  // the PV contribution of tile i-1 (relative to the old maximum) is in.
+  auto step = [&](int i, auto has_next_c, auto has_prev_c, f32x16 *s_in, f32x16 *s_out, bf16x8 (*p_in)[2],
+                  bf16x8 (*p_out)[2]) {
     constexpr bool HAS_NEXT = decltype(has_next_c)::value;
-    const int stage = (tile - t_beg) % A3_STAGES;
-    // tile+1 has landed (the only loads in flight) and every wave is done with
-    // tile-1, whose slot takes tile+2
+    constexpr bool HAS_PREV = decltype(has_prev_c)::value;
+    const int tile = t_beg + i;
     wait_vm_all();
     lds_barrier3();
-    if (tile + 2 < t_end) issue((tile - t_beg + 2) % A3_STAGES, tile + 2);
+    if (tile + 2 < t_end) issue((i + 2) % A3_STAGES, tile + 2);
     bf16x8 kf[2][5];
     if (HAS_NEXT) {
-      const char *ks = lds + ((tile - t_beg + 1) % A3_STAGES) * STAGE;
+      const char *ks = lds + ((i + 1) % A3_STAGES) * STAGE;
 #pragma unroll
       for (int st = 0; st < 2; ++st) {
         const char *krow = ks + (st * 32 + key_perm3(r32)) * (D * 2);
@@ -195,22 +199,28 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
         kf[st][4] = (g == 0) ? kf[st][4] : Mfma<bf16>::zero();
       }
     }
+    bf16x8 vf[2][2][3];
+    if (HAS_PREV) {
+      const char *vs = lds + ((i + A3_STAGES - 1) % A3_STAGES) * STAGE + KT_BYTES;
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+          for (int t = 0; t < 3; ++t) vf[st][c][t] = vfrag(vs, st * 32 + c * 16 + (tw >> 1) * 8, t);
+    }
 
     float tmax = -INFINITY;
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, s_cur[st][e]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    // lazy rescale: the reference maximum moves only when some query of the
-    // wave gained more than 2^8 over it
+      for (int e = 0; e < 16; ++e) tmax = fmaxf(tmax, s_in[st][e]);
+    tmax = half_swap_max(tmax);
     const float m_new = fmaxf(m_run, tmax);
-    if (__any((m_new - m_run) * c2 > 8.0f)) {
-      const float alpha = (m_run == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m_run - m_new) * c2);
-#pragma unroll
-      for (int t = 0; t < 3; ++t)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) o[t][e] *= alpha;
+    const bool resc = __any((m_new - m_run) * c2 > 8.0f);
+    float alpha = 1.0f;
+    if (resc) {
+      alpha = (m_run == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m_run - m_new) * c2);
       m_run = m_new;
     }
     const float mc = (m_run == -INFINITY) ? 0.0f : m_run * c2;
@@ -220,47 +230,72 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
       for (int c = 0; c < 5; ++c)
 #pragma unroll
         for (int st = 0; st < 2; ++st)
-          s_nxt[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st][c], qf[c], c == 0 ? zero16 : s_nxt[st], 0, 0, 0);
+          s_out[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st][c], qf[c], c == 0 ? zero16 : s_out[st], 0, 0, 0);
     }
-    bf16x8 pf[2][2];
+    if (HAS_PREV) {
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+          for (int t = 0; t < 3; ++t) o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[st][c][t], p_in[st][c], o[t], 0, 0, 0);
+    }
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int c = 0; c < 2; ++c)
 #pragma unroll
         for (int k = 0; k < 8; ++k)
-          pf[st][c][k] = (bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[st][c * 8 + k], c2, -mc));
-    if (HAS_NEXT) {
-      // one score MFMA, then a run of softmax VALU work, ten times
+          p_out[st][c][k] = (bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s_in[st][c * 8 + k], c2, -mc));
+    constexpr int NM = (HAS_NEXT ? 10 : 0) + (HAS_PREV ? 12 : 0);
+    if (NM > 0) {
+      // one MFMA, then a run of softmax VALU work
 #pragma unroll
-      for (int i = 0; i < 10; ++i) {
+      for (int j = 0; j < NM; ++j) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);  // VALU
+        __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // VALU
       }
     }
-
-    const char *vs = lds + stage * STAGE + KT_BYTES;
+    if (resc) {
+#pragma unroll
+      for (int t = 0; t < 3; ++t)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[t][e] *= alpha;
+    }
+  };
+  // PV of the last tile (its probabilities are in p_last)
+  auto drain = [&](int i, bf16x8 (*p_last)[2]) {
+    const char *vs = lds + (i % A3_STAGES) * STAGE + KT_BYTES;
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        const int kb = st * 32 + c * 16 + (tw >> 1) * 8;  // keys of lane group g = tw/2
+      for (int c = 0; c < 2; ++c)
 #pragma unroll
         for (int t = 0; t < 3; ++t)
-          o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(vs, kb, t), pf[st][c], o[t], 0, 0, 0);
-      }
+          o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vfrag(vs, st * 32 + c * 16 + (tw >> 1) * 8, t),
+                                                         p_last[st][c], o[t], 0, 0, 0);
   };
   f32x16 s_alt[2];
-  int tile = t_beg;
-  for (; tile + 2 < t_end; tile += 2) {
-    step(tile, std::true_type{}, s_cur, s_alt);
-    step(tile + 1, std::true_type{}, s_alt, s_cur);
+  bf16x8 pA[2][2], pB[2][2];
+  const int n = t_end - t_beg;
+  std::true_type T_;
+  std::false_type F_;
+  if (n > 1) step(0, T_, F_, s_cur, s_alt, pB, pA);
+  else step(0, F_, F_, s_cur, s_alt, pB, pA);
+  int i = 1;
+  for (; i + 2 < n; i += 2) {
+    step(i, T_, T_, s_alt, s_cur, pA, pB);
+    step(i + 1, T_, T_, s_cur, s_alt, pB, pA);
   }
-  if (tile + 1 < t_end) {
-    step(tile, std::true_type{}, s_cur, s_alt);
-    step(tile + 1, std::false_type{}, s_alt, s_cur);
+  if (i + 1 < n) {
+    step(i, T_, T_, s_alt, s_cur, pA, pB);
+    step(i + 1, F_, T_, s_cur, s_alt, pB, pA);
+    drain(i + 1, pA);
+  } else if (i < n) {
+    step(i, F_, T_, s_alt, s_cur, pA, pB);
+    drain(i, pB);
   } else {
-    step(tile, std::false_type{}, s_cur, s_alt);
+    drain(0, pA);
   }
 
   const float l_tot = __shfl(o[2][4], r32, 64);  // output row 72: the denominator

@@ -98,6 +98,29 @@ __device__ __forceinline__ int xcd_logical_id(int p, int T) {
   return off + (p >> 3);
 }
 
+// Maximum of v over the two 32-lane halves of a wave (lane l and l ^ 32),
+// exchanged by v_permlane32_swap in the vector ALU rather than through the
+// LDS queue, so it does not wait behind in-flight LDS reads.
+__device__ __forceinline__ float half_swap_max(float v) {
+  const unsigned u = __float_as_uint(v);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// Copy of 16 bytes per lane from global memory straight into LDS (lane i's
+// bytes land at lds_wave_base + 16 i; the base must be uniform over the
+// wave).  Issued as inline assembly so that the compiler does not see an
+// LDS write in flight and does not make every later LDS read wait for all
+// outstanding vector loads; the caller orders the copy against its readers
+// with explicit s_waitcnt vmcnt and a barrier.  M0 is written one wait state
+// before the load that reads it.
+__device__ __forceinline__ void lds_dma16(const void *gsrc, const void *lds_wave_base) {
+  const unsigned base = __builtin_amdgcn_readfirstlane(
+      (unsigned)(uintptr_t)(const __attribute__((address_space(3))) char *)lds_wave_base);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gsrc), "s"(base)
+               : "memory", "m0");
+}
+
 // Row r of the active set is packed as (chain << 16) | token.
 __device__ __forceinline__ int row_chain(int packed) { return packed >> 16; }
 __device__ __forceinline__ int row_token(int packed) { return packed & 0xFFFF; }
