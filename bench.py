@@ -84,10 +84,7 @@ def main():
     T = 20
     n_dense = 4                        # floor(0.2 * 20) dense steps, the rest reuse
     tgrid = synth.timestep_grid(T)
-    rng = np.random.default_rng([args.seed, 4242])
-    frac = args.frac if args.frac is not None else float(rng.uniform(0.10, 0.20))
-    n_blobs = int(rng.integers(1, 4))
-    mask = synth.blob_mask(shape.grid_h, shape.grid_w, frac, n_blobs, rng)
+    mask, frac, n_blobs = synth.c3_edit_region(args.seed, args.frac)
     idx = np.flatnonzero(mask)
     R = int(idx.size)
     log(f"workload: 1024px, {shape.layers} blocks, N={shape.tokens}, R={R} ({R / shape.tokens:.1%}), blobs={n_blobs}")

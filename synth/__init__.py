@@ -205,6 +205,18 @@ def blob_mask(gh: int, gw: int, frac: float, n_blobs: int, rng: np.random.Genera
     return m
 
 
+def c3_edit_region(seed: int = 0, frac=None):
+    """The 1024 px edit region of the benchmark workload: a seeded active
+    fraction in [0.10, 0.20] (unless `frac` is given) spread over 1-3 seeded
+    elliptical blobs of the 64 x 64 token grid.  Returns (mask, frac, n_blobs)."""
+    rng = np.random.default_rng([seed, 4242])
+    f = float(rng.uniform(0.10, 0.20))
+    if frac is not None:
+        f = float(frac)
+    n_blobs = int(rng.integers(1, 4))
+    return blob_mask(64, 64, f, n_blobs, rng), f, n_blobs
+
+
 def timestep_grid(T: int, t_max: int = 999) -> np.ndarray:
     """The sampler's integer timesteps, linearly spaced from t_max down to 0."""
     return np.round(np.linspace(t_max, 0, T)).astype(np.int64)

@@ -357,12 +357,18 @@ def test_determinism():
 
 
 @pytest.mark.timeout(400)
-def test_c3_reuse_step_full_size():
-    """1024 px (4096 tokens), 28 blocks, bf16, a 15 % blob mask, one reuse step
-    at the launch configuration the benchmark times."""
-    _say("c3 reuse full")
+@pytest.mark.parametrize("region", ["blob15", "bench"])
+def test_c3_reuse_step_full_size(region):
+    """1024 px (4096 tokens), 28 blocks, bf16, one reuse step: a 15 % two-blob
+    mask (614 rows), and the benchmark's own edit region (seed 0, 723 rows),
+    which runs every kernel in the launch configuration the benchmark times."""
+    _say("c3 reuse full", region)
     s = synth.shape_c3()
-    idx = np.flatnonzero(synth.blob_mask(64, 64, 0.15, 2, np.random.default_rng(0)))
+    if region == "bench":
+        idx = np.flatnonzero(synth.c3_edit_region(0)[0])
+        assert idx.size == 723
+    else:
+        idx = np.flatnonzero(synth.blob_mask(64, 64, 0.15, 2, np.random.default_rng(0)))
     got, refs, ctx = _reuse_case(s, 0, [idx], t=842, t_next=789)
     _check_reuse(s, got, refs, [idx], ctx)
 
