@@ -261,6 +261,35 @@ rc_status rc_reuse_step(rc_ctx *ctx, const rc_cache_view *cache, int32_t step,
 rc_status rc_update_cache(rc_ctx *ctx, const rc_cache_view *cache, int32_t step,
                           const rc_active_set *active, const void *active_hidden, void *stream);
 
+/* HOST-RESIDENT POOL (Sec. 3.4, pipelined execution).  The cache pool may
+ * live in pinned host memory (hipHostMalloc or torch pin_memory: page-locked
+ * and device-accessible; rc_cache_bytes and the slot layout are unchanged)
+ * when it does not fit in device memory.  A step then computes block l in
+ * entry l % 3 of a caller-owned device staging ring of
+ * rc_staging_bytes(ctx, batch) bytes: the copy engine uploads the keys and
+ * values of block l from the pool while earlier blocks compute, and after
+ * block l a small kernel writes the rows the step computed (keys, values and
+ * hidden state of every computed token) back into the pool while block l+1
+ * computes.  Both side streams are owned by the context (default priority),
+ * fork from `stream` at the start of the call and join it before the step's
+ * work on `stream` completes: the pool holds the step's results once
+ * `stream` has drained.  Results equal those of rc_reuse_step with
+ * RC_FUSE_UPDATE / rc_build_cache on a device pool of the same contents.
+ * bf16 storage only (RC_ERR_UNSUPPORTED otherwise); RC_ERR_INVALID_ARG if
+ * cache->base is not pinned host memory or staging is not device memory.
+ * All steps of one context that use the pool must run on one device.  The
+ * staging ring holds no state between calls. */
+size_t rc_staging_bytes(const rc_ctx *ctx, int32_t batch);
+rc_status rc_reuse_step_hosted(rc_ctx *ctx, const rc_cache_view *cache, int32_t step,
+                               const rc_active_set *active, const rc_step_io *io, void *staging,
+                               size_t staging_bytes, void *workspace, size_t workspace_bytes,
+                               void *stream);
+/* The dense step with the pool in host memory: nothing is uploaded, every
+ * row of every block is written back. */
+rc_status rc_build_cache_hosted(rc_ctx *ctx, const rc_cache_view *cache, int32_t step,
+                                const rc_step_io *io, void *staging, size_t staging_bytes,
+                                void *workspace, size_t workspace_bytes, void *stream);
+
 /* LOCALIZE REGION (Sec. 3.2): for each chain and delta column j, the map
  * a_j = maps[b][:, j] (device float32 [batch][N][n_delta], any positive
  * scale) is min-max normalised over the chain's tokens; token i joins the

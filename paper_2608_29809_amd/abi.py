@@ -96,6 +96,11 @@ def _load():
         "rc_reuse_step": (C.c_int, [P, C.POINTER(rc_cache_view), I32, C.POINTER(rc_active_set),
                                     C.POINTER(rc_step_io), P, U32, P, S, P]),
         "rc_update_cache": (C.c_int, [P, C.POINTER(rc_cache_view), I32, C.POINTER(rc_active_set), P, P]),
+        "rc_staging_bytes": (S, [P, I32]),
+        "rc_reuse_step_hosted": (C.c_int, [P, C.POINTER(rc_cache_view), I32, C.POINTER(rc_active_set),
+                                           C.POINTER(rc_step_io), P, S, P, S, P]),
+        "rc_build_cache_hosted": (C.c_int, [P, C.POINTER(rc_cache_view), I32, C.POINTER(rc_step_io), P, S, P, S,
+                                            P]),
         "rc_localize_region": (C.c_int, [P, P, I32, I32, C.c_float, I32, P, P, P, pI32, P]),
         "rc_maps_from_logits_scratch_bytes": (S, [I32, I32, I32]),
         "rc_maps_from_logits": (C.c_int, [P, I32, I32, I32, I32, pI32, I32, P, P, S, P]),
@@ -136,12 +141,14 @@ def _wrap(name):
 
 
 for _n in ["rc_create", "rc_cache_offsets", "rc_cache_latent_offset", "rc_prepare_text", "rc_build_cache",
-           "rc_reuse_step", "rc_update_cache", "rc_localize_region", "rc_maps_from_logits", "rc_compact_mask",
-           "rc_sync", "rc_set_kernel_timing", "rc_get_kernel_timing"]:
+           "rc_reuse_step", "rc_update_cache", "rc_reuse_step_hosted", "rc_build_cache_hosted",
+           "rc_localize_region", "rc_maps_from_logits", "rc_compact_mask", "rc_sync", "rc_set_kernel_timing",
+           "rc_get_kernel_timing"]:
     globals()[_n] = _wrap(_n)
 
 rc_destroy = LIB.rc_destroy
 rc_cache_bytes = LIB.rc_cache_bytes
 rc_text_kv_bytes = LIB.rc_text_kv_bytes
 rc_workspace_bytes = LIB.rc_workspace_bytes
+rc_staging_bytes = LIB.rc_staging_bytes
 rc_maps_from_logits_scratch_bytes = LIB.rc_maps_from_logits_scratch_bytes

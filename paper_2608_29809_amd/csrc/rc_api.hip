@@ -57,6 +57,10 @@ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 }  // namespace
 
+// Entries of the device staging ring of the host-resident pool (layers in
+// flight: one computing, one uploaded, one uploading).
+constexpr int kRing = 3;
+
 struct rc_ctx {
   rc_model_config cfg;
   rc_weights w;
@@ -69,6 +73,12 @@ struct rc_ctx {
   std::vector<Rec> recs;
   std::vector<hipEvent_t> pool;
   size_t pool_used = 0;
+  // host-resident pool: an upload stream and a write-back stream (default
+  // priority, created on first use on device pipe_device) and the events
+  // that order them against the caller's stream
+  int pipe_device = -1;
+  hipStream_t copy_s = nullptr, wb_s = nullptr;
+  hipEvent_t up_ev[kRing] = {}, wb_ev[kRing] = {}, cmp_ev = nullptr, fork_ev = nullptr, join_ev = nullptr;
 };
 
 namespace {
@@ -252,10 +262,62 @@ rc_status gemm(rc_ctx *c, int cls, const rc::GemmArgs &g, int epi, float *part, 
   }
 }
 
+// ------------------------------------------------------------------ host-resident pool
+
+// Pipelined execution with the cache pool in pinned host memory (Sec. 3.4):
+// block l computes in entry l % kRing of a device staging ring, whose keys
+// and values were uploaded from the pool by the copy engine while earlier
+// blocks computed; after block l the rows it computed (keys, values, hidden
+// state) are written back to the pool by a small kernel on a second stream
+// while block l+1 computes, and the freed entry takes the upload of block
+// l + kRing.  Events order the three streams; the caller's stream waits for
+// the last write-back before the step's work on it completes.
+struct HostPipe {
+  char *staging;       // device ring: kRing entries of `entry_bytes`
+  size_t entry_bytes;  // batch * slot bytes
+  const char *host;    // the pool, host address (uploads)
+};
+
+rc_status ensure_pipe(rc_ctx *c) {
+  int dev = -1;
+  RC_HIP(hipGetDevice(&dev));
+  if (c->copy_s) {
+    RC_CHECK(dev == c->pipe_device, RC_ERR_INVALID_ARG,
+             "host-resident steps of one context must run on one device (%d, now %d)", c->pipe_device, dev);
+    return RC_OK;
+  }
+  RC_HIP(hipStreamCreateWithFlags(&c->copy_s, hipStreamNonBlocking));
+  RC_HIP(hipStreamCreateWithFlags(&c->wb_s, hipStreamNonBlocking));
+  // the events inside a step only order work on this device (no host reads
+  // what they guard), so they skip the system-scope fence; the final join,
+  // after which the host may read the pool, keeps it
+  const unsigned order_only = hipEventDisableTiming | hipEventDisableSystemFence;
+  for (int r = 0; r < kRing; ++r) {
+    RC_HIP(hipEventCreateWithFlags(&c->up_ev[r], order_only));
+    RC_HIP(hipEventCreateWithFlags(&c->wb_ev[r], order_only));
+  }
+  RC_HIP(hipEventCreateWithFlags(&c->cmp_ev, order_only));
+  RC_HIP(hipEventCreateWithFlags(&c->fork_ev, order_only));
+  RC_HIP(hipEventCreateWithFlags(&c->join_ev, hipEventDisableTiming));
+  c->pipe_device = dev;
+  return RC_OK;
+}
+
+// Joins the write-back stream into the caller's stream when the step leaves
+// (also on an error return), so no write into the pool outlives the step.
+struct PipeJoin {
+  rc_ctx *c;
+  hipStream_t s;
+  bool forked = false;
+  ~PipeJoin() {
+    if (forked && hipEventRecord(c->join_ev, c->wb_s) == hipSuccess) (void)hipStreamWaitEvent(s, c->join_ev, 0);
+  }
+};
+
 template <typename T>
 rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_step_io *io, bool dense,
                    const rc_active_set *act, void *active_hidden, bool fuse, void *ws, size_t ws_bytes,
-                   hipStream_t s) {
+                   hipStream_t s, const HostPipe *hp = nullptr) {
   const int B = cache->batch, N = c->N, C = c->C, H = c->H, F = c->F, L = c->L, T_ = cache->steps;
   std::vector<int> counts(B);
   int R = 0, max_rb = 0;
@@ -365,15 +427,41 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
   }
 
   const bool emit = io->maps && io->n_delta > 0;
-  const long long slot_chain_stride = (long long)T_ * L * slot_elems(c);
+  // device pool: slot (b, step, l) in place; host-resident pool: entry
+  // l % kRing of the staging ring, chains one slot apart
+  const long long slot_chain_stride = hp ? (long long)slot_elems(c) : (long long)T_ * L * slot_elems(c);
   const size_t kv_half = (size_t)H * N * rc::kHeadDim;
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)rc::kHeadDim));
+
+  PipeJoin pipe_join{c, s};
+  auto upload = [&](int l) -> rc_status {  // keys and values of block l, every chain, on the copy stream
+    char *dst = hp->staging + (size_t)(l % kRing) * hp->entry_bytes;
+    for (int b = 0; b < B; ++b)
+      RC_HIP(hipMemcpyAsync(dst + (size_t)b * slot_elems(c) * c->esz, hp->host + slot_offset(c, T_, b, step, l),
+                            2 * kv_half * c->esz, hipMemcpyHostToDevice, c->copy_s));
+    RC_HIP(hipEventRecord(c->up_ev[l % kRing], c->copy_s));
+    return RC_OK;
+  };
+  if (hp) {
+    RC_TRY(ensure_pipe(c));
+    RC_HIP(hipEventRecord(c->fork_ev, s));  // earlier work on the caller's stream (and on the pool) first
+    RC_HIP(hipStreamWaitEvent(c->copy_s, c->fork_ev, 0));
+    RC_HIP(hipStreamWaitEvent(c->wb_s, c->fork_ev, 0));
+    pipe_join.forked = true;
+    if (!dense)  // a dense step recomputes every row: nothing to upload
+      for (int l = 0; l < std::min(kRing, L); ++l) RC_TRY(upload(l));
+  }
 
   bool a1_ready = false;  // the previous block's MLP reduction already wrote this block's LN1 rows
   for (int l = 0; l < L; ++l) {
     const rc_layer_weights &lw = c->layers[l];
-    T *slot = (T *)(cb + slot_offset(c, T_, 0, step, l));
+    T *slot = hp ? (T *)(hp->staging + (size_t)(l % kRing) * hp->entry_bytes)
+                 : (T *)(cb + slot_offset(c, T_, 0, step, l));
     T *Ks = slot, *Vs = slot + kv_half, *Hs = slot + 2 * kv_half;
+    if (hp) {
+      if (!dense) RC_HIP(hipStreamWaitEvent(s, c->up_ev[l % kRing], 0));  // this block's keys/values are in
+      else if (l >= kRing) RC_HIP(hipStreamWaitEvent(s, c->wb_ev[l % kRing], 0));  // the entry was written back
+    }
 
     if (!a1_ready)
       RC_TRY(timed(c, RC_KC_NORM, s, [&] { return rc::launch_ln_mod<T>(X, R, C, lw.sst, t0, 0, c->cfg.ln_eps, A1, s); }));
@@ -457,6 +545,20 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
         RC_TRY(gemm<T>(c, RC_KC_GEMM_FC2, g, rc::EPI_RESID, gpart, gpf, s, &ln, &a1_ready));
       } else {
         RC_TRY(gemm<T>(c, RC_KC_GEMM_FC2, g, rc::EPI_RESID, gpart, gpf, s));
+      }
+    }
+    if (hp) {  // write block l's rows back to the pool beside block l+1, then reuse the entry
+      const int r = l % kRing;
+      RC_HIP(hipEventRecord(c->cmp_ev, s));
+      RC_HIP(hipStreamWaitEvent(c->wb_s, c->cmp_ev, 0));
+      char *dst = cb + slot_offset(c, T_, 0, step, l);
+      RC_HIP(rc::launch_writeback_rows(rows, R, slot, (long long)slot_elems(c) * c->esz, dst,
+                                       (long long)T_ * L * slot_elems(c) * c->esz, H, N, C * (int)c->esz,
+                                       c->esz == 2, 64, c->wb_s));
+      RC_HIP(hipEventRecord(c->wb_ev[r], c->wb_s));
+      if (!dense && l + kRing < L) {
+        RC_HIP(hipStreamWaitEvent(c->copy_s, c->wb_ev[r], 0));
+        RC_TRY(upload(l + kRing));
       }
     }
   }
@@ -593,6 +695,19 @@ rc_status rc_create(const rc_model_config *cfg, const rc_weights *w, rc_ctx **ou
 void rc_destroy(rc_ctx *c) {
   if (!c) return;
   for (hipEvent_t e : c->pool) (void)hipEventDestroy(e);
+  if (c->copy_s) {
+    (void)hipStreamSynchronize(c->copy_s);
+    (void)hipStreamSynchronize(c->wb_s);
+    (void)hipStreamDestroy(c->copy_s);
+    (void)hipStreamDestroy(c->wb_s);
+    for (int r = 0; r < kRing; ++r) {
+      (void)hipEventDestroy(c->up_ev[r]);
+      (void)hipEventDestroy(c->wb_ev[r]);
+    }
+    (void)hipEventDestroy(c->cmp_ev);
+    (void)hipEventDestroy(c->fork_ev);
+    (void)hipEventDestroy(c->join_ev);
+  }
   delete c;
 }
 
@@ -715,6 +830,67 @@ rc_status rc_update_cache(rc_ctx *c, const rc_cache_view *cache, int32_t step, c
     }));
   }
   return RC_OK;
+}
+
+size_t rc_staging_bytes(const rc_ctx *c, int32_t batch) {
+  if (!c || batch < 1) return 0;
+  return (size_t)kRing * batch * slot_elems(c) * c->esz;
+}
+
+// Checks of a host-resident pool and its staging ring; on success `dev`
+// is the pool's view at its device-accessible address and `hp` the pipeline.
+static rc_status check_hosted(const rc_ctx *c, const rc_cache_view *cache, void *staging, size_t staging_bytes,
+                              rc_cache_view *dev, HostPipe *hp) {
+  RC_CHECK(c->esz == 2, RC_ERR_UNSUPPORTED, "the host-resident pool needs bf16 storage");
+  RC_CHECK(staging, RC_ERR_INVALID_ARG, "staging is null");
+  RC_CHECK(aligned16(staging), RC_ERR_ALIGN, "staging not 16-byte aligned");
+  const size_t entry = (size_t)cache->batch * slot_elems(c) * c->esz;
+  RC_CHECK(staging_bytes >= kRing * entry, RC_ERR_CAPACITY, "staging has %zu bytes, needs %zu", staging_bytes,
+           kRing * entry);
+  hipPointerAttribute_t ha{}, sa{};
+  const hipError_t eh = hipPointerGetAttributes(&ha, cache->base);
+  const hipError_t es = hipPointerGetAttributes(&sa, staging);
+  (void)hipGetLastError();  // a plain (unpinned) host pointer is reported as an error: not sticky, cleared
+  RC_CHECK(eh == hipSuccess && ha.type == hipMemoryTypeHost && ha.devicePointer, RC_ERR_INVALID_ARG,
+           "cache->base is not pinned, device-accessible host memory");
+  RC_CHECK(es == hipSuccess && sa.type == hipMemoryTypeDevice, RC_ERR_INVALID_ARG, "staging is not device memory");
+  *dev = *cache;
+  dev->base = ha.devicePointer;
+  hp->staging = (char *)staging;
+  hp->entry_bytes = entry;
+  hp->host = (const char *)cache->base;
+  return RC_OK;
+}
+
+rc_status rc_reuse_step_hosted(rc_ctx *c, const rc_cache_view *cache, int32_t step, const rc_active_set *active,
+                               const rc_step_io *io, void *staging, size_t staging_bytes, void *ws, size_t ws_bytes,
+                               void *stream) {
+  g_err.clear();
+  RC_CHECK(c, RC_ERR_INVALID_ARG, "ctx is null");
+  RC_TRY(check_cache(c, cache, step));
+  RC_TRY(check_io(c, io));
+  RC_TRY(check_active(c, cache, active));
+  RC_TRY(check_guided(io, cache->batch, active));
+  RC_CHECK(device_present(), RC_ERR_NO_DEVICE, "no HIP device");
+  rc_cache_view dev{};
+  HostPipe hp{};
+  RC_TRY(check_hosted(c, cache, staging, staging_bytes, &dev, &hp));
+  return run_step<bf16>(c, &dev, step, io, false, active, nullptr, true, ws, ws_bytes, (hipStream_t)stream, &hp);
+}
+
+rc_status rc_build_cache_hosted(rc_ctx *c, const rc_cache_view *cache, int32_t step, const rc_step_io *io,
+                                void *staging, size_t staging_bytes, void *ws, size_t ws_bytes, void *stream) {
+  g_err.clear();
+  RC_CHECK(c, RC_ERR_INVALID_ARG, "ctx is null");
+  RC_TRY(check_cache(c, cache, step));
+  RC_TRY(check_io(c, io));
+  RC_TRY(check_guided(io, cache->batch, nullptr));
+  RC_CHECK((long)cache->batch * c->N <= (1L << 30), RC_ERR_SHAPE, "batch too large");
+  RC_CHECK(device_present(), RC_ERR_NO_DEVICE, "no HIP device");
+  rc_cache_view dev{};
+  HostPipe hp{};
+  RC_TRY(check_hosted(c, cache, staging, staging_bytes, &dev, &hp));
+  return run_step<bf16>(c, &dev, step, io, true, nullptr, nullptr, true, ws, ws_bytes, (hipStream_t)stream, &hp);
 }
 
 rc_status rc_localize_region(rc_ctx *c, const float *maps, int32_t batch, int32_t n_delta, float threshold,

@@ -51,6 +51,12 @@ template <typename T>
 hipError_t launch_gemv(const void *W, const float *bias, const float *x, int N, int K, int silu_in, int silu_out,
                        float *y, hipStream_t s);
 template <typename T> hipError_t launch_final_ddim(const FinalArgs &a, hipStream_t s);
+// Copy of the key, value and hidden-state rows of `rows` (packed chain/token)
+// from a staging slot to a cache slot of the same layout (bf16 only; the
+// strides are between consecutive chains, in bytes).
+hipError_t launch_writeback_rows(const int *rows, int R, const void *stage, long long stage_chain_bytes, void *dst,
+                                 long long dst_chain_bytes, int heads, int tokens, int hidden_bytes, bool bf16_elems,
+                                 int workgroups, hipStream_t s);
 hipError_t launch_copy_chains(float *dst, long long dst_stride, const float *src, long long src_stride, int n, int B,
                               hipStream_t s);
 hipError_t launch_scatter_rows(const int *offsets, const int *idx, int B, const void *src, int R, int row_bytes,

@@ -382,6 +382,48 @@ hipError_t launch_copy_chains(float *dst, long long dst_stride, const float *src
   return hipGetLastError();
 }
 
+// Write-back of the rows a step computed from a device staging slot to the
+// same rows of a cache slot (the host-resident pool of the pipelined step):
+// for every packed row (chain << 16 | token), the token's key and value rows
+// of every head and its hidden-state row, in 16-byte vectors.  Consecutive
+// threads walk consecutive vectors of one row, so each hidden row is one
+// contiguous write and each key/value head row nine.  A grid-stride loop
+// keeps the workgroup count small: the copy runs beside the next block.
+__global__ __launch_bounds__(256) void writeback_rows_kernel(const int *rows, int R, const V16 *stage,
+                                                             long long stage_chain_vec, V16 *dst,
+                                                             long long dst_chain_vec, int heads, int tokens,
+                                                             int hidden_vec) {
+  constexpr int HV = kHeadDim * 2 / 16;  // 16-byte vectors per head row of 72 bf16
+  const int kv_vec = heads * HV;         // key (or value) vectors of one token
+  const int per_row = 2 * kv_vec + hidden_vec;
+  const long long half = (long long)heads * tokens * HV;  // vectors of the K (or V) array of one slot
+  const long total = (long)R * per_row;
+  for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < total; i += (long)gridDim.x * 256) {
+    const int r = (int)(i / per_row), v = (int)(i - (long)r * per_row);
+    const int pk = rows[r];
+    const long long cs = (long long)row_chain(pk), tok = row_token(pk);
+    long long off;
+    if (v < 2 * kv_vec) {
+      const int part = v / kv_vec, w = v - part * kv_vec, h = w / HV, e = w - h * HV;
+      off = part * half + ((long long)h * tokens + tok) * HV + e;
+    } else {
+      off = 2 * half + tok * hidden_vec + (v - 2 * kv_vec);
+    }
+    dst[cs * dst_chain_vec + off] = stage[cs * stage_chain_vec + off];
+  }
+}
+
+hipError_t launch_writeback_rows(const int *rows, int R, const void *stage, long long stage_chain_bytes, void *dst,
+                                 long long dst_chain_bytes, int heads, int tokens, int hidden_bytes, bool bf16_elems,
+                                 int workgroups, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  if (!bf16_elems || hidden_bytes % 16 || stage_chain_bytes % 16 || dst_chain_bytes % 16 || workgroups < 1)
+    return hipErrorInvalidValue;
+  rc_launch(writeback_rows_kernel, dim3(workgroups), dim3(256), 0, s, rows, R, (const V16 *)stage,
+            stage_chain_bytes / 16, (V16 *)dst, dst_chain_bytes / 16, heads, tokens, hidden_bytes / 16);
+  return hipGetLastError();
+}
+
 // H slot scatter: hslot(chain)[token][:] = src[r][:] for every active row,
 // 16-byte vectors; the chain of row r is found from the offsets.
 __global__ void scatter_rows_kernel(const int *offsets, const int *idx, int B, const V16 *src, int R,

@@ -56,10 +56,18 @@ class ActiveSet:
 
 
 class CacheBuffer:
-    def __init__(self, model: "RegionCacheModel", batch: int, steps: int):
+    """The cache pool: device memory, or with host=True pinned host memory
+    (the host-resident pool of the pipelined step; accessors then return
+    host tensors)."""
+
+    def __init__(self, model: "RegionCacheModel", batch: int, steps: int, host: bool = False):
         nbytes = abi.rc_cache_bytes(model.ctx, batch, steps)
         self.model = model
-        self.buf = torch.empty(nbytes, dtype=torch.uint8, device=model.device)
+        self.host = host
+        if host:
+            self.buf = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+        else:
+            self.buf = torch.empty(nbytes, dtype=torch.uint8, device=model.device)
         self.view = abi.rc_cache_view(self.buf.data_ptr(), nbytes, batch, steps)
         self.batch, self.steps = batch, steps
 
@@ -149,8 +157,15 @@ class RegionCacheModel:
             pass
 
     # ------------------------------------------------------------ buffers
-    def alloc_cache(self, batch: int, steps: int) -> CacheBuffer:
-        return CacheBuffer(self, batch, steps)
+    def alloc_cache(self, batch: int, steps: int, host: bool = False) -> CacheBuffer:
+        return CacheBuffer(self, batch, steps, host)
+
+    def staging(self, batch: int) -> torch.Tensor:
+        """Device staging ring of the host-resident pool."""
+        nbytes = abi.rc_staging_bytes(self.ctx, batch)
+        if getattr(self, "_stage", None) is None or self._stage.numel() < nbytes:
+            self._stage = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        return self._stage
 
     def workspace(self, max_rows: int, batch: int) -> torch.Tensor:
         nbytes = abi.rc_workspace_bytes(self.ctx, max_rows, batch)
@@ -194,7 +209,12 @@ class RegionCacheModel:
         io, keep = self._io(inp, timestep, timestep_next, tkv, delta, maps, latent_out, t_vec, text_valid,
                             guidance)
         ws = self.workspace(cache.batch * self.N, cache.batch)
-        abi.rc_build_cache(self.ctx, C.byref(cache.view), step, C.byref(io), _ptr(ws), ws.numel(), _stream())
+        if cache.host:
+            st = self.staging(cache.batch)
+            abi.rc_build_cache_hosted(self.ctx, C.byref(cache.view), step, C.byref(io), _ptr(st), st.numel(),
+                                      _ptr(ws), ws.numel(), _stream())
+        else:
+            abi.rc_build_cache(self.ctx, C.byref(cache.view), step, C.byref(io), _ptr(ws), ws.numel(), _stream())
 
     def reuse_step(self, cache: CacheBuffer, step: int, act: ActiveSet, inp: torch.Tensor, timestep: int,
                    timestep_next: int, tkv: torch.Tensor, delta=None, maps=None, latent_out=None, t_vec=None,
@@ -204,8 +224,15 @@ class RegionCacheModel:
                             guidance)
         ws = self.workspace(max(act.total, 1), cache.batch)
         s = act.struct()
-        abi.rc_reuse_step(self.ctx, C.byref(cache.view), step, C.byref(s), C.byref(io), _ptr(active_hidden),
-                          abi.RC_FUSE_UPDATE if fuse else 0, _ptr(ws), ws.numel(), _stream())
+        if cache.host:
+            if not fuse or active_hidden is not None:
+                raise ValueError("a host-resident pool is updated in place (fuse=True, no active_hidden)")
+            st = self.staging(cache.batch)
+            abi.rc_reuse_step_hosted(self.ctx, C.byref(cache.view), step, C.byref(s), C.byref(io), _ptr(st),
+                                     st.numel(), _ptr(ws), ws.numel(), _stream())
+        else:
+            abi.rc_reuse_step(self.ctx, C.byref(cache.view), step, C.byref(s), C.byref(io), _ptr(active_hidden),
+                              abi.RC_FUSE_UPDATE if fuse else 0, _ptr(ws), ws.numel(), _stream())
 
     def update_cache(self, cache: CacheBuffer, step: int, act: ActiveSet, active_hidden: torch.Tensor):
         s = act.struct()

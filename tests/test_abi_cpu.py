@@ -205,6 +205,31 @@ def test_text_and_update_validation(ctx):
     assert abi.LIB.rc_update_cache(ctx, C.byref(view), 2, C.byref(a), FAKE, None) == -2
 
 
+def test_hosted_pool_validation(ctx):
+    """Host-resident pool: the staging ring holds three entries of every
+    chain's slot; the hosted steps validate like the device ones before any
+    device call, and refuse fp32 storage."""
+    N, C_ = 1024, 1152
+    assert abi.rc_staging_bytes(ctx, 2) == 3 * 2 * 3 * N * C_ * 2
+    assert abi.rc_staging_bytes(ctx, 0) == 0
+    nb = abi.rc_cache_bytes(ctx, 1, 4)
+    view = abi.rc_cache_view(FAKE, nb, 1, 4)
+    ws = abi.rc_workspace_bytes(ctx, 1024, 1)
+    sb = abi.rc_staging_bytes(ctx, 1)
+    h = (C.c_int32 * 2)(0, 7)
+    a = abi.rc_active_set(FAKE, FAKE, C.cast(h, C.POINTER(C.c_int32)), 1)
+    reuse, build = abi.LIB.rc_reuse_step_hosted, abi.LIB.rc_build_cache_hosted
+    assert reuse(None, C.byref(view), 1, C.byref(a), C.byref(_io()), FAKE, sb, FAKE, ws, None) == -1
+    assert reuse(ctx, C.byref(view), 4, C.byref(a), C.byref(_io()), FAKE, sb, FAKE, ws, None) == -2
+    bad = (C.c_int32 * 2)(0, 2000)
+    ab = abi.rc_active_set(FAKE, FAKE, C.cast(bad, C.POINTER(C.c_int32)), 1)
+    assert reuse(ctx, C.byref(view), 1, C.byref(ab), C.byref(_io()), FAKE, sb, FAKE, ws, None) == -4
+    assert build(ctx, C.byref(view), 0, C.byref(_io(timestep=1000)), FAKE, sb, FAKE, ws, None) == -1
+    if NO_GPU:
+        assert reuse(ctx, C.byref(view), 1, C.byref(a), C.byref(_io()), FAKE, sb, FAKE, ws, None) == -6
+        assert build(ctx, C.byref(view), 0, C.byref(_io()), FAKE, sb, FAKE, ws, None) == -6
+
+
 def test_kernel_timing_classes(ctx):
     abi.rc_set_kernel_timing(ctx, 1)
     ms, n = C.c_double(), C.c_int64()
