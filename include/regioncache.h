@@ -164,7 +164,9 @@ const char *rc_last_error(void);
 
 /* Validate the config, copy it and the weight pointers into a host-side
  * context.  Touches no device.  RC_ERR_UNSUPPORTED for shapes outside the
- * list above. */
+ * list above.  A context holds host-side state (timing records and, once a
+ * host-resident step has run, its side streams and events): calls on one
+ * context must not overlap from several host threads. */
 rc_status rc_create(const rc_model_config *config, const rc_weights *weights, rc_ctx **out);
 void rc_destroy(rc_ctx *ctx);
 
