@@ -452,6 +452,14 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       for (int l = 0; l < std::min(kRing, L); ++l) RC_TRY(upload(l));
   }
 
+  // Weights of a block's later GEMMs are warmed into the memory-side cache
+  // by earlier kernels of the block (each warming kernel pays for its extra
+  // loads, so the pairs are the measured winners): for a region step the
+  // out-projections and the MLP-down weights, warmed by GEMMs; for a dense
+  // step also the cross query and MLP-up weights and the next block's QKV
+  // weights, warmed by the attention kernels and the MLP-up GEMM.
+  auto wlines = [&](long long n, long long k) { return n * k * (long long)c->esz / 128; };
+  const long long fc2_lines = wlines(C, F), fc2_half = fc2_lines / 2;
   bool a1_ready = false;  // the previous block's MLP reduction already wrote this block's LN1 rows
   for (int l = 0; l < L; ++l) {
     const rc_layer_weights &lw = c->layers[l];
@@ -471,6 +479,7 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       g.A = A1; g.W = lw.qkv_w; g.bias = lw.qkv_b; g.M = R; g.N = 3 * C; g.K = C; g.lda = C;
       g.out = Q; g.ldo = C; g.rows = rows; g.kslot = Ks; g.vslot = Vs;
       g.chain_stride = slot_chain_stride; g.tokens = N; g.hidden = C;
+      g.warm = lw.proj_w; g.warm_lines = wlines(C, C);
       RC_TRY(gemm<T>(c, RC_KC_GEMM_QKV, g, rc::EPI_QKV, gpart, gpf, s));
     }
     {  // region-level sparse self-attention over the whole slot
@@ -478,6 +487,7 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       a.Q = Q; a.K = Ks; a.V = Vs; a.v_rowmajor = 1; a.chain_stride = slot_chain_stride; a.head_stride = (long long)N * rc::kHeadDim;
       a.offsets = offsets_dev; a.n_keys = N; a.n_valid = N; a.hidden = C; a.splits = splits;
       a.O = O; a.Opart = part; a.ML = ml; a.total_rows = R; a.scale_log2 = scale_log2;
+      if (dense) { a.warm = lw.xq_w; a.warm_lines = wlines(C, C); }
       RC_TRY(timed(c, RC_KC_ATTN_SELF, s, [&] {
         return sizeof(T) == 2 ? rc::launch_attention3(a, B, max_rb, s)
                               : rc::launch_attention<T>(a, B, max_rb, false, s);
@@ -492,11 +502,14 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       rc::GemmArgs g{};
       g.A = O; g.W = lw.proj_w; g.bias = lw.proj_b; g.M = R; g.N = C; g.K = C; g.lda = C;
       g.X = X; g.ldx = C; g.gate = lw.sst + 2 * C; g.gate2 = t0 + 2 * C; g.xt = A1;
+      g.warm = lw.xproj_w; g.warm_lines = wlines(C, C);
       RC_TRY(gemm<T>(c, RC_KC_GEMM_PROJ, g, rc::EPI_RESID, gpart, gpf, s));
     }
     {  // cross-attention query
       rc::GemmArgs g{};
       g.A = A1; g.W = lw.xq_w; g.bias = lw.xq_b; g.M = R; g.N = C; g.K = C; g.lda = C; g.out = Q; g.ldo = C;
+      if (dense) { g.warm = lw.fc1_w; g.warm_lines = wlines(F, C); }
+      else { g.warm = lw.fc2_w; g.warm_lines = fc2_half; }
       RC_TRY(gemm<T>(c, RC_KC_GEMM_XQ, g, rc::EPI_STORE, gpart, gpf, s));
     }
     {  // cross-attention to the text, emitting the delta-token maps
@@ -507,6 +520,7 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       a.offsets = offsets_dev; a.n_keys = c->Mp; a.n_valid = c->M; a.text_valid = io->text_valid;
       a.hidden = C; a.splits = 1;
       a.O = O; a.total_rows = R; a.scale_log2 = scale_log2;
+      if (dense) { a.warm = lw.fc2_w; a.warm_lines = fc2_lines; }
       if (emit) {
         a.n_delta = io->n_delta;
         for (int j = 0; j < io->n_delta; ++j) a.delta[j] = io->delta_cols_host[j];
@@ -525,12 +539,14 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       rc::GemmArgs g{};
       g.A = O; g.W = lw.xproj_w; g.bias = lw.xproj_b; g.M = R; g.N = C; g.K = C; g.lda = C;
       g.X = X; g.ldx = C;
+      if (!dense) { g.warm = (const char *)lw.fc2_w + fc2_half * 128; g.warm_lines = fc2_lines - fc2_half; }
       RC_TRY(gemm<T>(c, RC_KC_GEMM_XPROJ, g, rc::EPI_RESID, gpart, gpf, s));
     }
     RC_TRY(timed(c, RC_KC_NORM, s, [&] { return rc::launch_ln_mod<T>(X, R, C, lw.sst, t0, 3, c->cfg.ln_eps, A1, s); }));
     {  // MLP up + GELU
       rc::GemmArgs g{};
       g.A = A1; g.W = lw.fc1_w; g.bias = lw.fc1_b; g.M = R; g.N = F; g.K = C; g.lda = C; g.out = G; g.ldo = F;
+      if (dense && l + 1 < L) { g.warm = c->layers[l + 1].qkv_w; g.warm_lines = wlines(3 * C, C); }
       RC_TRY(gemm<T>(c, RC_KC_GEMM_FC1, g, rc::EPI_GELU, gpart, gpf, s));
     }
     {  // MLP down + gate + residual; merge into the cached hidden state

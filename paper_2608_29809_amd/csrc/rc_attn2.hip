@@ -43,14 +43,15 @@ __device__ __forceinline__ void wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-template <bool CROSS, int STAGES>
+// WARM: also warm a.warm into the memory-side cache (a separate instantiation).
+template <bool CROSS, int STAGES, bool WARM>
 __global__ __launch_bounds__(256, 2) void attn2_kernel(AttnArgs a) {
   constexpr int D = kHeadDim;
   constexpr int KT_BYTES = A2_BK * D * 2;      // 9216: K tile [64][72]
   constexpr int VT_BYTES = D * A2_BK * 2;      // 9216: V^T tile [72][64]
   constexpr int STAGE = KT_BYTES + VT_BYTES;
   constexpr int K_CH = KT_BYTES / 16;          // 576 chunks
-  __shared__ __attribute__((aligned(1024))) char lds[STAGES * STAGE + 128];
+  __shared__ __attribute__((aligned(1024))) char lds[STAGES * STAGE + 128 + (WARM ? 256 : 0)];
   // a row of 64 bf16 ones: row 72 of the V^T operand, so that output row 72
   // of O^T accumulates sum_k P[k] -- the softmax denominator, with the same
   // rounded probabilities as the numerator
@@ -75,6 +76,7 @@ __global__ __launch_bounds__(256, 2) void attn2_kernel(AttnArgs a) {
   const int t_beg = (int)((long)split * n_tiles / a.splits), t_end = (int)((long)(split + 1) * n_tiles / a.splits);
   const bf16 *Kg = (const bf16 *)a.K + b * a.chain_stride + h * a.head_stride;
   const bf16 *Vg = (const bf16 *)a.V + b * a.chain_stride + h * a.head_stride;  // transposed [72][n_keys]
+  if (WARM && wave == 0) warm_lines(a.warm, a.warm_lines, p, T, lds + STAGES * STAGE + 128);
 
   auto issue = [&](int stage, int tile) {
     char *ks = lds + stage * STAGE, *vs = ks + KT_BYTES;
@@ -291,7 +293,8 @@ hipError_t launch_attention2(const AttnArgs &a, int n_chains, int max_rows, hipS
   if (max_rows <= 0) return hipSuccess;
   if (a.n_keys % A2_BK != 0 || a.splits < 1 || a.splits > a.n_keys / A2_BK || a.v_rowmajor) return hipErrorInvalidValue;
   dim3 grid((max_rows + A2_BQ - 1) / A2_BQ, (a.hidden / kHeadDim) * a.splits, n_chains);
-  rc_launch(attn2_kernel<true, 2>, grid, dim3(256), 0, s, a);
+  if (a.warm && a.warm_lines > 0) rc_launch(attn2_kernel<true, 2, true>, grid, dim3(256), 0, s, a);
+  else rc_launch(attn2_kernel<true, 2, false>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

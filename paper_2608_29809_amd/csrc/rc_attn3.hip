@@ -39,13 +39,16 @@ __device__ __forceinline__ int key_perm3(int m) {
 __device__ __forceinline__ void lds_barrier3() { asm volatile("s_barrier" ::: "memory"); }
 __device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// WARM: also warm a.warm into the memory-side cache (a separate instantiation,
+// so that the kernel without it carries none of its code or LDS).
+template <bool WARM>
 __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
   constexpr int D = kHeadDim;
   constexpr int KT_BYTES = A3_BK * D * 2;  // K tile [64][72]
   constexpr int VT_BYTES = A3_BK * D * 2;  // V tile [64][72]
   constexpr int STAGE = KT_BYTES + VT_BYTES;
   constexpr int K_CH = KT_BYTES / 16;      // 576 16-byte chunks per operand tile
-  __shared__ __attribute__((aligned(1024))) char lds[A3_STAGES * STAGE + 16];
+  __shared__ __attribute__((aligned(1024))) char lds[A3_STAGES * STAGE + 16 + (WARM ? 256 : 0)];
   // two 4-element chunks read in place of value dims >= 72: (1, 0, 0, 0), so
   // that output row 72 of O^T accumulates sum_k P[k] -- the softmax
   // denominator, with the same rounded probabilities as the numerator -- and
@@ -66,6 +69,7 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
   const int t_beg = (int)((long)split * n_tiles / a.splits), t_end = (int)((long)(split + 1) * n_tiles / a.splits);
   const bf16 *Kg = (const bf16 *)a.K + b * a.chain_stride + h * a.head_stride;
   const bf16 *Vg = (const bf16 *)a.V + b * a.chain_stride + h * a.head_stride;  // [n_keys][72]
+  if (WARM && wave == 0) warm_lines(a.warm, a.warm_lines, p, T, lds + A3_STAGES * STAGE + 16);
 
   auto issue = [&](int stage, int tile) {
     char *ks = lds + stage * STAGE, *vs = ks + KT_BYTES;
@@ -397,7 +401,8 @@ hipError_t launch_attention3(const AttnArgs &a, int n_chains, int max_rows, hipS
   if (a.n_keys % A3_BK != 0 || a.splits < 1 || a.splits > a.n_keys / A3_BK || !a.v_rowmajor)
     return hipErrorInvalidValue;
   dim3 grid((max_rows + A3_BQ - 1) / A3_BQ, (a.hidden / kHeadDim) * a.splits, n_chains);
-  rc_launch(attn3_kernel, grid, dim3(256), 0, s, a);
+  if (a.warm && a.warm_lines > 0) rc_launch(attn3_kernel<true>, grid, dim3(256), 0, s, a);
+  else rc_launch(attn3_kernel<false>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -121,6 +121,28 @@ __device__ __forceinline__ void lds_dma16(const void *gsrc, const void *lds_wave
                : "memory", "m0");
 }
 
+// Memory-side cache warm-up of a buffer a later kernel reads: one dword of
+// each 128-byte line is copied into a 256-byte LDS scratch of the calling
+// wave that nothing reads, so no register is held; the lines are then
+// served from the Infinity Cache instead of HBM.  Caller `part` of `parts`
+// (one wave per workgroup) covers its contiguous share of the lines.  Called
+// before the kernel's own first loads: loads retire in order, so the
+// kernel's first vmcnt waits also retire these copies (the warming kernel
+// pays for part of their latency), and the calling wave has waited for them
+// before it ends, as it waits for its own LDS copies.
+__device__ __forceinline__ void warm_lines(const void *p, long long lines, long long part, long long parts,
+                                           const void *lds_wave_scratch) {
+  if (lines <= 0) return;
+  const unsigned base = __builtin_amdgcn_readfirstlane(
+      (unsigned)(uintptr_t)(const __attribute__((address_space(3))) char *)lds_wave_scratch);
+  const long long per = (lines + parts - 1) / parts, l0 = part * per, l1 = min(l0 + per, lines);
+  for (long long i = l0 + (threadIdx.x & 63); i < l1; i += 64) {
+    const char *src = (const char *)p + i * 128;
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off" ::"v"(src), "s"(base)
+                 : "memory", "m0");
+  }
+}
+
 // Row r of the active set is packed as (chain << 16) | token.
 __device__ __forceinline__ int row_chain(int packed) { return packed >> 16; }
 __device__ __forceinline__ int row_token(int packed) { return packed & 0xFFFF; }

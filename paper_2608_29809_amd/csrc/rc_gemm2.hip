@@ -171,7 +171,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
   constexpr int PASSES = (BM * CLD * 4 <= GROUP_BYTES) ? 1 : 2;
   constexpr int HB = BM / PASSES;
   static_assert(HB * CLD * 4 <= GROUP_BYTES && HB % WM == 0, "an output band must fit a group's ring");
-  __shared__ __attribute__((aligned(1024))) char lds[KG * GROUP_BYTES];
+  __shared__ __attribute__((aligned(1024))) char lds[KG * GROUP_BYTES + 256];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int kgrp = wave / NW, w4 = wave % NW;
@@ -192,6 +192,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
   const int tm = grp * GM + idx % gm, tn = idx / gm;
   const int m0 = tm * BM, n0 = tn * BN;
   // K group kgrp covers its own contiguous share of this split's K range
+  if (wave == 0) warm_lines(g.warm, g.warm_lines, p, T, lds + KG * GROUP_BYTES);
   const int kps_g = k_per_split / KG;
   const int kbeg = kz * k_per_split + kgrp * kps_g;
   const int nk = kps_g / G2_BK;

@@ -41,6 +41,9 @@ struct GemmArgs {
   void *tkv;        // entry (layer, chain 0)
   int text_len, text_pad;
   long long tkv_chain_stride;
+  // buffer a later kernel reads, warmed into the memory-side cache (or null)
+  const void *warm;
+  long long warm_lines;  // 128-byte lines
 };
 
 struct AttnArgs {
@@ -65,6 +68,8 @@ struct AttnArgs {
   int delta[8];
   float *pmaps;          // [heads][R][n_delta]
   float scale_log2;      // log2(e)/sqrt(72)
+  const void *warm;      // buffer a later kernel reads, warmed into the memory-side cache (or null)
+  long long warm_lines;  // 128-byte lines
 };
 
 template <typename T> hipError_t launch_gemm(const GemmArgs &a, int epi, hipStream_t s);

@@ -324,6 +324,54 @@ def test_dense_step_two_chains():
         assert relerr(to_np(out)[b], ref["latent_next"]) < 2e-2
 
 
+@pytest.mark.gpu
+@pytest.mark.timeout(400)
+def test_dense_step_full_grid():
+    """Build-cache (dense) step at 1024 px: 4096 tokens of one chain, two
+    blocks, as the benchmark's dense step launches them (4096-row GEMMs on
+    128 x 128 tiles two stages deep, the unsplit MLP-down GEMM, 4096-query
+    self-attention) against the oracle, maps included."""
+    _say("dense step, 4096 tokens")
+    s = synth.ModelShape(layers=2, grid_h=64, grid_w=64, dtype="bf16")
+    W = synth.make_weights(s, seed=9)
+    txt = synth.make_text(s, 1, 9)
+    lat = synth.make_latent(s, 1, 9)
+    model = RegionCacheModel(s, W)
+    cache = model.alloc_cache(1, 2)
+    tkv = model.prepare_text(model.to_storage(txt))
+    delta = [2, 40, 77, 119]
+    maps = torch.zeros((1, s.tokens, len(delta)), device="cuda")
+    out = torch.empty(lat.shape, device="cuda")
+    model.build_cache(cache, 0, torch.from_numpy(lat).cuda(), 950, 900, tkv, delta, maps, out)
+    torch.cuda.synchronize()
+    got = download_slot(cache, 0, s.layers, 1)
+    ref = O.dense_step(s, W, lat[0], 950, 900, oracle_text_kv(s, W, txt[0]), np.array(delta))
+    for k in ("H", "K", "V"):
+        e = relerr(got[k][:, 0], ref[k])
+        _say(k, e)
+        assert e < 2e-2
+    e_l, e_m = relerr(to_np(out)[0], ref["latent_next"]), relerr(to_np(maps)[0], ref["maps"])
+    _say("latent", e_l, "maps", e_m)
+    assert e_l < 2e-2 and e_m < 2e-2
+
+
+@pytest.mark.gpu
+@pytest.mark.timeout(400)
+def test_four_chains_mixed_fractions():
+    """Four 1024 px chains whose edit regions cover about 5, 10, 25 and 50 % of
+    their tokens (blob masks), two blocks: the batch-of-four workload's row
+    count (over 3072 rows, so the large-row tile plans and the unsplit
+    MLP-down GEMM run on the reuse path) and four chains' keys in one
+    attention launch."""
+    s = synth.ModelShape(layers=2, grid_h=64, grid_w=64, dtype="bf16")
+    per = [np.flatnonzero(synth.blob_mask(64, 64, f, 2, np.random.default_rng(20 + i)))
+           for i, f in enumerate((0.05, 0.10, 0.25, 0.50))]
+    _say("four chains", [p.size for p in per])
+    assert sum(p.size for p in per) > 3072
+    got, refs, ctx = _reuse_case(s, 12, per, t=640, t_next=590)
+    _check_reuse(s, got, refs, per, ctx)
+
+
 def test_empty_mask_and_poison():
     """No active token: slot unchanged and latent = cached trajectory.  Then
     NaN in the stale cached rows of the active tokens never reaches an output."""
