@@ -517,7 +517,9 @@ static void launch_reduce(const GemmArgs &a, int epi, int splits, const float *p
 // 256 CUs in one wave of workgroups takes the largest tile that still fills
 // them, with eight waves (32x32 or 32x64 / 64x32 per wave) where the tile
 // allows it; grids of one to two waves of 64-row tiles keep 64x128 with two
-// workgroups per CU.  Split-K over the grid pays only for K = 4608.
+// workgroups per CU.  Split-K over the grid pays only for K = 4608, in two
+// halves up to ~2700 rows (the halves as 128-row tiles while they fit one
+// wave of workgroups); three splits measured slower in the step at 4096 rows.
 GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats) {
   GemmPlan p{64, 128, 1, 1, 2, 2, 2};
   const int nk = K / G2_BK;
@@ -534,7 +536,8 @@ GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats) {
       else set(64, 2, 3, 2, 2);
     } else if (t64 < 384 && nk % 2 == 0 && room) {
       p.splits = 2;
-      set(64, 1, 3, 2, 4);
+      if (t128 * 2 <= 256) set(128, 1, 3, 2, 4);
+      else set(64, 1, 2, 2, 2);
     }
     return p;
   }
