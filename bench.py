@@ -471,9 +471,7 @@ def sweep_leg(model1, args):
     out = {}
     steps = list(range(4, T))
     for f in (0.05, 0.10, 0.25, 0.50, 1.00):
-        rng = np.random.default_rng([args.seed, int(f * 1000)])
-        per = [np.flatnonzero(synth.blob_mask(64, 64, f, int(rng.integers(1, 4)), rng)) for _ in range(B)]
-        act = ActiveSet.from_lists(per)
+        act = ActiveSet.from_lists(synth.sweep_regions(args.seed, f, B))
 
         def rs(k, act=act):
             s = steps[k % len(steps)]

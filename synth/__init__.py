@@ -217,6 +217,14 @@ def c3_edit_region(seed: int = 0, frac=None):
     return blob_mask(64, 64, f, n_blobs, rng), f, n_blobs
 
 
+def sweep_regions(seed: int, frac: float, chains: int = 4):
+    """Active token lists of the batch active-fraction workload at 1024 px:
+    per chain a blob mask of 1-3 seeded blobs covering `frac` of the 64 x 64
+    grid.  Returns a list of ascending index arrays."""
+    rng = np.random.default_rng([seed, int(frac * 1000)])
+    return [np.flatnonzero(blob_mask(64, 64, frac, int(rng.integers(1, 4)), rng)) for _ in range(chains)]
+
+
 def timestep_grid(T: int, t_max: int = 999) -> np.ndarray:
     """The sampler's integer timesteps, linearly spaced from t_max down to 0."""
     return np.round(np.linspace(t_max, 0, T)).astype(np.int64)

@@ -372,6 +372,57 @@ def test_four_chains_mixed_fractions():
     _check_reuse(s, got, refs, per, ctx)
 
 
+@pytest.mark.gpu
+@pytest.mark.timeout(400)
+@pytest.mark.parametrize("frac", [0.05, 0.10, 0.50])
+def test_fraction_sweep_workloads(frac):
+    """The batch active-fraction workload (four 1024 px chains with the masks
+    the benchmark's sweep draws: 820, 1640 and 8192 rows) in its launch
+    configuration, two blocks, against the oracle."""
+    s = synth.ModelShape(layers=2, grid_h=64, grid_w=64, dtype="bf16")
+    per = synth.sweep_regions(0, frac)
+    _say("fraction sweep", frac, [p.size for p in per])
+    got, refs, ctx = _reuse_case(s, 13, per, t=700, t_next=650)
+    _check_reuse(s, got, refs, per, ctx)
+
+
+@pytest.mark.gpu
+@pytest.mark.timeout(400)
+def test_all_active_four_chains_equals_dense():
+    """The 100 % point of the batch sweep at full size: four 1024 px chains,
+    28 blocks, every token active (16384 rows).  The region step over a slot
+    whose keys, values and hidden states were poisoned equals the dense step
+    bit for bit (slot, maps, latents)."""
+    _say("all-active, four chains, 28 blocks")
+    s = synth.shape_c3()
+    B = 4
+    W = synth.make_weights(s, seed=14)
+    txt = synth.make_text(s, B, 14)
+    lat = torch.from_numpy(synth.make_latent(s, B, 14)).cuda()
+    model = RegionCacheModel(s, W)
+    cache = model.alloc_cache(B, 2)
+    tkv = model.prepare_text(model.to_storage(txt))
+    delta = [1, 60, 118]
+    maps = torch.zeros((B, s.tokens, 3), device="cuda")
+    out = torch.empty_like(lat)
+    model.build_cache(cache, 0, lat, 920, 870, tkv, delta, maps, out)
+    cache2 = model.alloc_cache(B, 2)
+    cache2.buf.copy_(cache.buf)
+    for b in range(B):
+        for l in range(s.layers):
+            cache2.K(b, 0, l).fill_(float("nan"))
+            cache2.V(b, 0, l).fill_(float("nan"))
+            cache2.H(b, 0, l).fill_(float("nan"))
+    maps2 = torch.zeros_like(maps)
+    out2 = torch.empty_like(out)
+    model.reuse_step(cache2, 0, ActiveSet.from_lists([np.arange(s.tokens)] * B), lat, 920, 870, tkv, delta, maps2,
+                     out2)
+    torch.cuda.synchronize()
+    assert torch.equal(cache2.buf, cache.buf)
+    assert torch.equal(out2, out) and torch.equal(maps2, maps)
+    assert torch.isfinite(out).all() and bool((maps > 0).all())
+
+
 def test_empty_mask_and_poison():
     """No active token: slot unchanged and latent = cached trajectory.  Then
     NaN in the stale cached rows of the active tokens never reaches an output."""
