@@ -413,8 +413,7 @@ def resolution_leg(W, args):
         tkv = model.prepare_text(model.to_storage(txt))
         lat = torch.from_numpy(synth.make_latent(shape, 1, args.seed + 2)).cuda()
         nxt = torch.empty_like(lat)
-        rng = np.random.default_rng([args.seed, px])
-        act = ActiveSet.from_lists([np.flatnonzero(synth.blob_mask(g, g, 0.15, 2, rng))])
+        act = ActiveSet.from_lists([synth.resolution_region(args.seed, g)])
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
 
         def timed(fn, n=6):

@@ -225,6 +225,14 @@ def sweep_regions(seed: int, frac: float, chains: int = 4):
     return [np.flatnonzero(blob_mask(64, 64, frac, int(rng.integers(1, 4)), rng)) for _ in range(chains)]
 
 
+def resolution_region(seed: int, g: int, frac: float = 0.15):
+    """Active token list of the resolution workload on a g x g token grid
+    (g = 32, 64, 128 for 512, 1024, 2048 px): two seeded blobs covering
+    `frac` of the grid."""
+    rng = np.random.default_rng([seed, g * 16])
+    return np.flatnonzero(blob_mask(g, g, frac, 2, rng))
+
+
 def timestep_grid(T: int, t_max: int = 999) -> np.ndarray:
     """The sampler's integer timesteps, linearly spaced from t_max down to 0."""
     return np.round(np.linspace(t_max, 0, T)).astype(np.int64)

@@ -486,14 +486,65 @@ def test_c3_reuse_step_full_size(region):
 
 @pytest.mark.gpu
 @pytest.mark.timeout(400)
-def test_reuse_step_2048px():
-    """2048 px (128 x 128 = 16384 tokens), two blocks, a 10 % blob region: the
-    largest grid the library takes, keys of all 16384 tokens per head."""
-    _say("2048 px reuse")
+@pytest.mark.parametrize("region", ["blob10", "bench15"])
+def test_reuse_step_2048px(region):
+    """2048 px (128 x 128 = 16384 tokens), two blocks: a 10 % blob region and
+    the benchmark's resolution-workload region (15 %, 2458 rows): the largest
+    grid the library takes, keys of all 16384 tokens per head."""
+    _say("2048 px reuse", region)
     s = synth.ModelShape(layers=2, grid_h=128, grid_w=128, dtype="bf16")
-    idx = np.flatnonzero(synth.blob_mask(128, 128, 0.10, 2, np.random.default_rng(3)))
+    if region == "bench15":
+        idx = synth.resolution_region(0, 128)
+        assert idx.size == 2458
+    else:
+        idx = np.flatnonzero(synth.blob_mask(128, 128, 0.10, 2, np.random.default_rng(3)))
     got, refs, ctx = _reuse_case(s, 3, [idx], t=600, t_next=550)
     _check_reuse(s, got, refs, [idx], ctx)
+
+
+@pytest.mark.gpu
+@pytest.mark.timeout(400)
+def test_dense_step_2048px_sampled_rows():
+    """Dense step at 2048 px (16384 tokens, two blocks), as the resolution
+    workload launches it: the first block's keys and values of 256 sampled
+    tokens against the oracle evaluated row by row (patch and position
+    embedding, LayerNorm, modulation, QKV projection), and the all-active
+    region step over a poisoned slot equal to the dense step bit for bit."""
+    _say("2048 px dense, sampled rows")
+    s = synth.ModelShape(layers=2, grid_h=128, grid_w=128, dtype="bf16")
+    W = synth.make_weights(s, seed=15)
+    txt = synth.make_text(s, 1, 15)
+    lat = synth.make_latent(s, 1, 15)
+    model = RegionCacheModel(s, W)
+    cache = model.alloc_cache(1, 2)
+    tkv = model.prepare_text(model.to_storage(txt))
+    lat_d = torch.from_numpy(lat).cuda()
+    out = torch.empty_like(lat_d)
+    model.build_cache(cache, 0, lat_d, 810, 760, tkv, latent_out=out)
+    torch.cuda.synchronize()
+    rows = np.sort(np.random.default_rng(15).choice(s.tokens, 256, replace=False))
+    C, H, D = s.hidden, s.heads, s.head_dim
+    t0 = O.adaln_single(W, O.timestep_embedding(W, 810))
+    lw = W["layers"][0]
+    mod = O.layer_modulation(lw, t0)
+    X = O.patch_embed(W, lat[0], s.grid_h, s.grid_w, s.patch)[rows]
+    qkv = O.modulate(O.layer_norm(X), mod[0], mod[1]) @ lw["qkv_w"].astype(np.float64).T + lw["qkv_b"]
+    k_ref = qkv[:, C:2 * C].reshape(-1, H, D).transpose(1, 0, 2)
+    v_ref = qkv[:, 2 * C:].reshape(-1, H, D).transpose(1, 0, 2)
+    e_k = relerr(to_np(cache.K(0, 0, 0))[:, rows], k_ref)
+    e_v = relerr(to_np(cache.V(0, 0, 0))[:, rows], v_ref)
+    _say(f"block 0 sampled rows: K {e_k:.2e} V {e_v:.2e}")
+    assert e_k < 2e-2 and e_v < 2e-2
+    cache2 = model.alloc_cache(1, 2)
+    cache2.buf.copy_(cache.buf)
+    for l in range(s.layers):
+        cache2.K(0, 0, l).fill_(float("nan"))
+        cache2.V(0, 0, l).fill_(float("nan"))
+        cache2.H(0, 0, l).fill_(float("nan"))
+    out2 = torch.empty_like(out)
+    model.reuse_step(cache2, 0, ActiveSet.from_lists([np.arange(s.tokens)]), lat_d, 810, 760, tkv, latent_out=out2)
+    torch.cuda.synchronize()
+    assert torch.equal(cache2.buf, cache.buf) and torch.equal(out2, out)
 
 
 @pytest.mark.gpu
