@@ -61,7 +61,7 @@ def log(*a):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: only --gpus 1 is supported; this build runs on one GPU (asked for {args.gpus})",
+        print(f"bench.py: only --gpus 1 is supported; the library runs one process on one GPU (asked for {args.gpus})",
               file=sys.stderr)
         sys.exit(2)
     import torch
