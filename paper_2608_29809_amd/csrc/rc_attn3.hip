@@ -179,20 +179,28 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
 
   // One key tile i (tile = t_beg + i): wait for tile i+1 and recycle the slot
   // of tile i-2 for tile i+2, update the running maximum with tile i's
-  // scores, then one interleaved block: the score MFMAs of tile i+1 and the
+  // scores, then a run of MFMA groups: the score MFMAs of tile i+1, then the
   // PV MFMAs of tile i-1 (probabilities from the previous step, values still
-  // in their ring slot) run while the vector ALUs exponentiate tile i.  A
-  // rescale of the reference maximum is applied to o after the block, once
-  // the PV contribution of tile i-1 (relative to the old maximum) is in.
+  // in their ring slot), one MFMA per group, each group also taking its
+  // share of tile i's exponentials (and, under the score MFMAs, the value
+  // fragment reads), so that the vector ALU works while the matrix core
+  // runs.  Group boundaries are scheduling barriers, and each exponential's
+  // operand and result pass through an empty asm so that the compiler keeps
+  // it inside its group instead of batching all of them before or after the
+  // MFMAs.  A rescale of the reference maximum is applied to o after the
+  // groups, once the PV contribution of tile i-1 (relative to the old
+  // maximum) is in; every output element sees the same operations in the
+  // same order as a tile-by-tile loop.
   auto step = [&](int i, auto has_next_c, auto has_prev_c, f32x16 *s_in, f32x16 *s_out, bf16x8 (*p_in)[2],
                   bf16x8 (*p_out)[2]) {
     constexpr bool HAS_NEXT = decltype(has_next_c)::value;
     constexpr bool HAS_PREV = decltype(has_prev_c)::value;
+    constexpr int NS = HAS_NEXT ? 10 : 0, NP = HAS_PREV ? 12 : 0, NG = NS + NP;
     const int tile = t_beg + i;
     wait_vm_all();
     lds_barrier3();
     if (tile + 2 < t_end) issue((i + 2) % A3_STAGES, tile + 2);
-    bf16x8 kf[2][5];
+    bf16x8 kf[2][5];  // key fragments of tile i+1, consumed in (c, st) order
     if (HAS_NEXT) {
       const char *ks = lds + ((i + 1) % A3_STAGES) * STAGE;
 #pragma unroll
@@ -200,18 +208,14 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
         const char *krow = ks + (st * 32 + key_perm3(r32)) * (D * 2);
 #pragma unroll
         for (int c = 0; c < 5; ++c) kf[st][c] = *(const bf16x8 *)(krow + (c * 16 + g * 8) * 2);
-        kf[st][4] = (g == 0) ? kf[st][4] : Mfma<bf16>::zero();
       }
     }
-    bf16x8 vf[2][2][3];
-    if (HAS_PREV) {
-      const char *vs = lds + ((i + A3_STAGES - 1) % A3_STAGES) * STAGE + KT_BYTES;
+    const char *vs = lds + ((i + A3_STAGES - 1) % A3_STAGES) * STAGE + KT_BYTES;
+    bf16x8 vf[12];  // value fragment k = (st, c, t) = (k / 6, k / 3 % 2, k % 3) of tile i-1
+    auto vread = [&](int k) { vf[k] = vfrag(vs, (k / 6) * 32 + ((k / 3) % 2) * 16 + (tw >> 1) * 8, k % 3); };
+    if (HAS_PREV && !HAS_NEXT) {
 #pragma unroll
-      for (int st = 0; st < 2; ++st)
-#pragma unroll
-        for (int c = 0; c < 2; ++c)
-#pragma unroll
-          for (int t = 0; t < 3; ++t) vf[st][c][t] = vfrag(vs, st * 32 + c * 16 + (tw >> 1) * 8, t);
+      for (int k = 0; k < 12; ++k) vread(k);
     }
 
     float tmax = -INFINITY;
@@ -222,44 +226,45 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
     tmax = half_swap_max(tmax);
     const float m_new = fmaxf(m_run, tmax);
     const bool resc = __any((m_new - m_run) * c2 > 8.0f);
-    float alpha = 1.0f;
-    if (resc) {
-      alpha = (m_run == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m_run - m_new) * c2);
-      m_run = m_new;
-    }
+    const float alpha = (m_run == -INFINITY) ? 0.0f : __builtin_amdgcn_exp2f((m_run - m_new) * c2);
+    m_run = resc ? m_new : m_run;
     const float mc = (m_run == -INFINITY) ? 0.0f : m_run * c2;
+    __builtin_amdgcn_sched_barrier(0);
 
-    if (HAS_NEXT) {
+    float pe[32];  // exponentials of tile i, element st*16 + c*8 + k
 #pragma unroll
-      for (int c = 0; c < 5; ++c)
+    for (int j = 0; j < NG; ++j) {
+      if (j < NS) {
+        const int c = j / 2, st = j % 2;
+        // d0 = 72 lies past the row (it reads the next row); zeroed without a branch
+        const bf16x8 kk = (c == 4 && g == 1) ? Mfma<bf16>::zero() : kf[st][c];
+        s_out[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kk, qf[c], c == 0 ? zero16 : s_out[st], 0, 0, 0);
+        if (HAS_PREV) vread(j);
+      } else {
+        const int k = j - NS;
+        o[k % 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[k], p_in[k / 6][(k / 3) % 2], o[k % 3], 0, 0, 0);
+        if (HAS_NEXT && j < 12) vread(j);
+      }
+      const int e0 = 32 * j / NG, e1 = 32 * (j + 1) / NG;
 #pragma unroll
-        for (int st = 0; st < 2; ++st)
-          s_out[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st][c], qf[c], c == 0 ? zero16 : s_out[st], 0, 0, 0);
+      for (int e = e0; e < e1; ++e) {
+        float x = __builtin_fmaf(s_in[e / 16][e % 16], c2, -mc);
+        asm volatile("" : "+v"(x));
+        pe[e] = __builtin_amdgcn_exp2f(x);
+        asm volatile("" : "+v"(pe[e]));
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
-    if (HAS_PREV) {
+    if (NG == 0) {
 #pragma unroll
-      for (int st = 0; st < 2; ++st)
-#pragma unroll
-        for (int c = 0; c < 2; ++c)
-#pragma unroll
-          for (int t = 0; t < 3; ++t) o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[st][c][t], p_in[st][c], o[t], 0, 0, 0);
+      for (int e = 0; e < 32; ++e) pe[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s_in[e / 16][e % 16], c2, -mc));
     }
 #pragma unroll
     for (int st = 0; st < 2; ++st)
 #pragma unroll
       for (int c = 0; c < 2; ++c)
 #pragma unroll
-        for (int k = 0; k < 8; ++k)
-          p_out[st][c][k] = (bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s_in[st][c * 8 + k], c2, -mc));
-    constexpr int NM = (HAS_NEXT ? 10 : 0) + (HAS_PREV ? 12 : 0);
-    if (NM > 0) {
-      // one MFMA, then a run of softmax VALU work
-#pragma unroll
-      for (int j = 0; j < NM; ++j) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // VALU
-      }
-    }
+        for (int k = 0; k < 8; ++k) p_out[st][c][k] = (bf16)pe[st * 16 + c * 8 + k];
     if (resc) {
 #pragma unroll
       for (int t = 0; t < 3; ++t)
