@@ -114,7 +114,9 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
 
   const f32x16 zero16 = {};  // C operand of a tile's first score MFMA, kept live
   // S^T of one tile: lane group g, sub-tile st, accumulator e = c*8 + k  <->
-  // key st*32 + c*16 + g*8 + k
+  // key st*32 + c*16 + g*8 + k.  For c = 4 the g = 1 lanes read dims 72..79,
+  // i.e. the first dims of the next key row (or of value row 0): finite
+  // values multiplied by the zero query dims 72..79, adding exact zeros.
   auto scores = [&](int stage, f32x16 *s) {
     const char *ks = lds + stage * STAGE;
     bf16x8 kf[2][5];
@@ -123,8 +125,6 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
       const char *krow = ks + (st * 32 + key_perm3(r32)) * (D * 2);
 #pragma unroll
       for (int c = 0; c < 5; ++c) kf[st][c] = *(const bf16x8 *)(krow + (c * 16 + g * 8) * 2);
-      // d0 = 72 lies past the row (it reads the next row); zero it without a branch
-      kf[st][4] = (g == 0) ? kf[st][4] : Mfma<bf16>::zero();
     }
 #pragma unroll
     for (int c = 0; c < 5; ++c)
@@ -236,9 +236,7 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
     for (int j = 0; j < NG; ++j) {
       if (j < NS) {
         const int c = j / 2, st = j % 2;
-        // d0 = 72 lies past the row (it reads the next row); zeroed without a branch
-        const bf16x8 kk = (c == 4 && g == 1) ? Mfma<bf16>::zero() : kf[st][c];
-        s_out[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kk, qf[c], c == 0 ? zero16 : s_out[st], 0, 0, 0);
+        s_out[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st][c], qf[c], c == 0 ? zero16 : s_out[st], 0, 0, 0);
         if (HAS_PREV) vread(j);
       } else {
         const int k = j - NS;
