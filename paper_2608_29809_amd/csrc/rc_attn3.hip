@@ -232,6 +232,9 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
     __builtin_amdgcn_sched_barrier(0);
 
     float pe[32];  // exponentials of tile i, element st*16 + c*8 + k
+    // the wave in its MFMA groups takes issue priority over the other wave
+    // of its SIMD (in its barrier wait or conversion tail)
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int j = 0; j < NG; ++j) {
       if (j < NS) {
@@ -253,6 +256,7 @@ __global__ __launch_bounds__(256, 2) void attn3_kernel(AttnArgs a) {
       }
       __builtin_amdgcn_sched_barrier(0);
     }
+    __builtin_amdgcn_s_setprio(0);
     if (NG == 0) {
 #pragma unroll
       for (int e = 0; e < 32; ++e) pe[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s_in[e / 16][e % 16], c2, -mc));
