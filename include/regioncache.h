@@ -325,15 +325,19 @@ rc_status rc_compact_mask(const uint8_t *mask, int32_t batch, int32_t tokens, in
 /* Wait for `stream`; returns RC_ERR_HIP if any enqueued work failed. */
 rc_status rc_sync(void *stream);
 
-/* Per-kernel timing for profiling: while enabled, every launch of the
- * context is bracketed by a pair of HIP events on its stream.  Query returns
- * the summed duration (ms) and launch count of one kernel class since
- * enabling (it synchronises).  Classes are the RC_KC_* values. */
+/* Per-kernel timing for profiling: while enabled, every operation of the
+ * context is bracketed by a pair of HIP events on its stream, stamped by the
+ * dispatches of its first and last kernel; every class is one kernel per
+ * operation except RC_KC_MISC.  Query returns the summed duration (ms) and
+ * operation count of one kernel class since enabling (it synchronises).
+ * Classes are the RC_KC_* values. */
 enum {
   RC_KC_GEMM = 0, RC_KC_ATTN_SELF = 1, RC_KC_ATTN_CROSS = 2, RC_KC_ATTN_COMBINE = 3,
   RC_KC_NORM = 4, RC_KC_EMBED = 5, RC_KC_FINAL = 6, RC_KC_COND = 7, RC_KC_MISC = 8,
   RC_KC_GEMM_QKV = 9, RC_KC_GEMM_FC1 = 10, RC_KC_GEMM_FC2 = 11, RC_KC_GEMM_PROJ = 12,
-  RC_KC_GEMM_XQ = 13, RC_KC_GEMM_XPROJ = 14, RC_KC_COUNT = 15
+  RC_KC_GEMM_XQ = 13, RC_KC_GEMM_XPROJ = 14,
+  RC_KC_SPLIT_FINISH = 15, /* sum of a split-K GEMM's partials (+ the next block's LayerNorm) */
+  RC_KC_COUNT = 16
 };
 rc_status rc_set_kernel_timing(rc_ctx *ctx, int32_t enable);
 rc_status rc_get_kernel_timing(rc_ctx *ctx, int32_t kernel_class, double *total_ms, int64_t *launches);

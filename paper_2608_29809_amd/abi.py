@@ -21,11 +21,11 @@ RC_F32, RC_BF16 = 0, 1
 RC_FUSE_UPDATE = 1
 (RC_KC_GEMM, RC_KC_ATTN_SELF, RC_KC_ATTN_CROSS, RC_KC_ATTN_COMBINE, RC_KC_NORM, RC_KC_EMBED,
  RC_KC_FINAL, RC_KC_COND, RC_KC_MISC, RC_KC_GEMM_QKV, RC_KC_GEMM_FC1, RC_KC_GEMM_FC2, RC_KC_GEMM_PROJ,
- RC_KC_GEMM_XQ, RC_KC_GEMM_XPROJ) = range(15)
-RC_KC_COUNT = 15
+ RC_KC_GEMM_XQ, RC_KC_GEMM_XPROJ, RC_KC_SPLIT_FINISH) = range(16)
+RC_KC_COUNT = 16
 KERNEL_CLASSES = ["gemm", "attn_self", "attn_cross", "attn_combine", "norm", "embed", "final",
                   "cond", "misc", "gemm_qkv", "gemm_fc1", "gemm_fc2", "gemm_proj",
-                  "gemm_xq", "gemm_xproj"]
+                  "gemm_xq", "gemm_xproj", "split_finish"]
 
 
 class RcError(RuntimeError):

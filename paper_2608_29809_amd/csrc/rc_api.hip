@@ -256,7 +256,9 @@ rc_status gemm(rc_ctx *c, int cls, const rc::GemmArgs &g, int epi, float *part, 
   if (ln_done) *ln_done = false;
   if constexpr (sizeof(T) == 2) {
     const rc::GemmPlan pl = rc::plan_gemm2(g.M, g.N, g.K, part ? part_floats : 0);
-    return timed(c, cls, s, [&] { return rc::launch_gemm2(g, epi, pl, part, s, ln, ln_done); });
+    RC_TRY(timed(c, cls, s, [&] { return rc::launch_gemm2(g, epi, pl, part, s); }));
+    if (pl.splits == 1) return RC_OK;
+    return timed(c, RC_KC_SPLIT_FINISH, s, [&] { return rc::launch_gemm2_finish(g, epi, pl, part, s, ln, ln_done); });
   } else {
     return timed(c, cls, s, [&] { return rc::launch_gemm<T>(g, epi, s); });
   }

@@ -554,9 +554,7 @@ GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats) {
   return p;
 }
 
-hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &pl, float *partial, hipStream_t s,
-                        const LnNext *ln, bool *ln_done) {
-  if (ln_done) *ln_done = false;
+hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &pl, float *partial, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
   if (pl.bn != 128 || a.N % 128 || a.K % (G2_BK * pl.splits * pl.kg)) return hipErrorInvalidValue;
   const bool split = pl.splits > 1;
@@ -583,8 +581,13 @@ hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &pl, float *p
     default: return hipErrorInvalidValue;
   }
 #undef RC_G2
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || !split) return e;
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm2_finish(const GemmArgs &a, int epi, const GemmPlan &pl, const float *partial, hipStream_t s,
+                               const LnNext *ln, bool *ln_done) {
+  if (ln_done) *ln_done = false;
+  if (a.M <= 0 || pl.splits <= 1) return hipSuccess;
   if (ln && epi == EPI_RESID && a.N % 4 == 0 && a.N <= 4 * 256 * 2 && pl.splits <= 4) {
     const dim3 grid(a.M), block(256);
     const float *pp = partial;

@@ -91,11 +91,14 @@ struct LnNext {
   float eps;
   void *out;  // [M][N] E
 };
-// With `ln` non-null and a split plan, the split reduction of an EPI_RESID
-// GEMM also applies `ln` (one pass over each finished row); *ln_done tells
-// the caller whether it did.
-hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &plan, float *partial, hipStream_t s,
-                        const LnNext *ln = nullptr, bool *ln_done = nullptr);
+// The tiles of a bf16 GEMM; with a split plan they write fp32 partials,
+// which launch_gemm2_finish then sums.
+hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &plan, float *partial, hipStream_t s);
+// Sum of a split plan's partials with the epilogue.  With `ln` non-null the
+// reduction of an EPI_RESID GEMM also applies `ln` (one pass over each
+// finished row); *ln_done tells the caller whether it did.
+hipError_t launch_gemm2_finish(const GemmArgs &a, int epi, const GemmPlan &plan, const float *partial,
+                               hipStream_t s, const LnNext *ln = nullptr, bool *ln_done = nullptr);
 template <typename T> hipError_t launch_attention(const AttnArgs &a, int n_chains, int max_rows,
                                                   bool emit_maps, hipStream_t s);
 // bf16 cross-attention to the transposed text values, emitting the
