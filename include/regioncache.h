@@ -316,6 +316,27 @@ rc_status rc_maps_from_logits(const void *logits, int32_t n_layers, int32_t head
                               int32_t text_len, const int32_t *delta_cols_host, int32_t n_delta,
                               float *maps_out, void *partial, size_t partial_bytes, void *stream);
 
+/* ALLOCATION-FREE VARIANT of rc_maps_from_logits, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same computation and results, with
+ * the per-layer partial maps in a library-owned static device array of
+ * RC_STATIC_SCRATCH_BYTES instead of the caller's `partial`.  Each GPU the
+ * library runs on holds its own copy of that array until the process ends;
+ * its address is looked up once per device on the first call there.  The
+ * call allocates and frees nothing.
+ *   - n_layers*tokens*n_delta*4 must not exceed RC_STATIC_SCRATCH_BYTES
+ *     (16 MiB: up to 32 layers x 16384 tokens x 8 delta columns), else
+ *     RC_ERR_CAPACITY before any launch.  Other arguments as above.
+ *   - Every call on one GPU shares the array and leaves its contents behind;
+ *     each call overwrites the part it reads before reading it, so nothing
+ *     needs clearing.  Calls that overlap on one GPU (several streams or
+ *     host threads without ordering) race on the array: their maps are
+ *     undefined.  Order such calls on one stream. */
+#define RC_STATIC_SCRATCH_BYTES ((size_t)16 << 20)
+rc_status rc_maps_from_logits_noalloc(const void *logits, int32_t n_layers, int32_t heads, int32_t tokens,
+                                      int32_t text_len, const int32_t *delta_cols_host, int32_t n_delta,
+                                      float *maps_out, void *stream);
+
 /* Stable compaction of masks [batch][tokens] (device u8, nonzero = active)
  * into idx (device, capacity batch*tokens) and offsets [batch+1] (device);
  * offsets_host as in rc_localize_region. */

@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -56,6 +57,14 @@ inline bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 }  // namespace
+
+// Library-owned scratch of the allocation-free maps call
+// (rc_maps_from_logits_noalloc): the per-layer partial maps, at most
+// kStaticScratchBytes.  Every GPU the library runs on holds its own copy
+// until the process ends.  In host code `scratch` names a host-side stand-in,
+// not device memory: kernels get the address static_scratch() looks up.
+constexpr size_t kStaticScratchBytes = (size_t)16 << 20;
+static __device__ __align__(256) char scratch[kStaticScratchBytes];
 
 // Entries of the device staging ring of the host-resident pool (layers in
 // flight: one computing, one uploaded, one uploading).
@@ -643,6 +652,56 @@ bool device_present() {
   return hipGetDeviceCount(&n) == hipSuccess && n > 0;
 }
 
+// Arguments of the maps-from-logits calls (everything but the scratch).
+rc_status check_maps_args(const void *logits, int n_layers, int heads, int tokens, int text_len,
+                          const int32_t *delta_cols_host, int n_delta, const float *maps_out) {
+  RC_CHECK(logits && delta_cols_host && maps_out, RC_ERR_INVALID_ARG, "null argument");
+  RC_CHECK(aligned16(logits), RC_ERR_ALIGN, "logits not 16-byte aligned");
+  RC_CHECK(n_layers >= 1 && heads >= 1, RC_ERR_SHAPE, "n_layers/heads must be positive");
+  RC_CHECK(tokens >= 64 && tokens % 64 == 0, RC_ERR_UNSUPPORTED, "tokens %d must be a positive multiple of 64",
+           tokens);
+  RC_CHECK(text_len >= 8 && text_len <= 128 && text_len % 8 == 0, RC_ERR_UNSUPPORTED,
+           "text_len %d must be a multiple of 8 in [8, 128]", text_len);
+  RC_CHECK(n_delta >= 1 && n_delta <= 8, RC_ERR_INVALID_ARG, "n_delta %d outside [1, 8]", n_delta);
+  for (int j = 0; j < n_delta; ++j)
+    RC_CHECK(delta_cols_host[j] >= 0 && delta_cols_host[j] < text_len, RC_ERR_INDEX, "delta column %d out of range",
+             delta_cols_host[j]);
+  RC_CHECK(tokens <= (1 << 24) && n_layers <= (1 << 16), RC_ERR_SHAPE, "tokens %d / n_layers %d too large", tokens,
+           n_layers);
+  return RC_OK;
+}
+
+// Per-layer partial maps (one kernel) summed over layers in order (another).
+rc_status launch_maps(const void *logits, int n_layers, int heads, int tokens, int text_len,
+                      const int32_t *delta_cols_host, int n_delta, float *maps_out, float *partial, hipStream_t s) {
+  RC_HIP(rc::launch_maps_from_logits((const uint16_t *)logits, n_layers, heads, tokens, text_len, delta_cols_host,
+                                     n_delta, partial, s));
+  RC_HIP(rc::launch_sum_partials(partial, n_layers, tokens * n_delta, maps_out, s));
+  return RC_OK;
+}
+
+// Device address of the static scratch array on the current device, looked
+// up once per device (each GPU holds its own copy of the array, at its own
+// address).  Host code uses only this address, never the array's name.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+rc_status static_scratch(void **out) {
+  int dev = -1;
+  RC_HIP(hipGetDevice(&dev));
+  RC_CHECK(dev >= 0 && dev < kMaxDevices, RC_ERR_UNSUPPORTED, "device %d outside the library's table", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    RC_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    RC_CHECK(p, RC_ERR_HIP, "hipGetSymbolAddress returned a null address");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return RC_OK;
+}
+
 }  // namespace
 
 // ====================================================================== C ABI
@@ -942,25 +1001,29 @@ rc_status rc_maps_from_logits(const void *logits, int32_t n_layers, int32_t head
                               const int32_t *delta_cols_host, int32_t n_delta, float *maps_out, void *partial,
                               size_t partial_bytes, void *stream) {
   g_err.clear();
-  RC_CHECK(logits && delta_cols_host && maps_out && partial, RC_ERR_INVALID_ARG, "null argument");
-  RC_CHECK(aligned16(logits), RC_ERR_ALIGN, "logits not 16-byte aligned");
-  RC_CHECK(n_layers >= 1 && heads >= 1, RC_ERR_SHAPE, "n_layers/heads must be positive");
-  RC_CHECK(tokens >= 64 && tokens % 64 == 0, RC_ERR_UNSUPPORTED, "tokens %d must be a positive multiple of 64",
-           tokens);
-  RC_CHECK(text_len >= 8 && text_len <= 128 && text_len % 8 == 0, RC_ERR_UNSUPPORTED,
-           "text_len %d must be a multiple of 8 in [8, 128]", text_len);
-  RC_CHECK(n_delta >= 1 && n_delta <= 8, RC_ERR_INVALID_ARG, "n_delta %d outside [1, 8]", n_delta);
-  for (int j = 0; j < n_delta; ++j)
-    RC_CHECK(delta_cols_host[j] >= 0 && delta_cols_host[j] < text_len, RC_ERR_INDEX, "delta column %d out of range",
-             delta_cols_host[j]);
+  RC_TRY(check_maps_args(logits, n_layers, heads, tokens, text_len, delta_cols_host, n_delta, maps_out));
+  RC_CHECK(partial, RC_ERR_INVALID_ARG, "null argument");
   const size_t need = rc_maps_from_logits_scratch_bytes(n_layers, tokens, n_delta);
   RC_CHECK(partial_bytes >= need, RC_ERR_CAPACITY, "scratch has %zu bytes, needs %zu", partial_bytes, need);
   RC_CHECK(device_present(), RC_ERR_NO_DEVICE, "no HIP device");
-  hipStream_t s = (hipStream_t)stream;
-  RC_HIP(rc::launch_maps_from_logits((const uint16_t *)logits, n_layers, heads, tokens, text_len, delta_cols_host,
-                                     n_delta, (float *)partial, s));
-  RC_HIP(rc::launch_sum_partials((const float *)partial, n_layers, tokens * n_delta, maps_out, s));
-  return RC_OK;
+  return launch_maps(logits, n_layers, heads, tokens, text_len, delta_cols_host, n_delta, maps_out, (float *)partial,
+                     (hipStream_t)stream);
+}
+
+rc_status rc_maps_from_logits_noalloc(const void *logits, int32_t n_layers, int32_t heads, int32_t tokens,
+                                      int32_t text_len, const int32_t *delta_cols_host, int32_t n_delta,
+                                      float *maps_out, void *stream) {
+  g_err.clear();
+  RC_TRY(check_maps_args(logits, n_layers, heads, tokens, text_len, delta_cols_host, n_delta, maps_out));
+  const size_t need = rc_maps_from_logits_scratch_bytes(n_layers, tokens, n_delta);
+  RC_CHECK(need <= kStaticScratchBytes, RC_ERR_CAPACITY,
+           "n_layers*tokens*n_delta*4 = %zu bytes exceeds the library's static scratch of %zu bytes", need,
+           kStaticScratchBytes);
+  RC_CHECK(device_present(), RC_ERR_NO_DEVICE, "no HIP device");
+  void *sp = nullptr;
+  RC_TRY(static_scratch(&sp));
+  return launch_maps(logits, n_layers, heads, tokens, text_len, delta_cols_host, n_delta, maps_out, (float *)sp,
+                     (hipStream_t)stream);
 }
 
 rc_status rc_compact_mask(const uint8_t *mask, int32_t batch, int32_t tokens, int32_t *idx, int32_t *offsets,

@@ -192,6 +192,19 @@ def test_localize_and_logits_validation(ctx):
     if NO_GPU:
         assert ml(FAKE, 28, 16, 4096, 120, dp, 2, FAKE, FAKE, sb, None) == -6
         assert abi.LIB.rc_sync(None) == -6
+    # the allocation-free variant: same argument checks, and problems beyond
+    # its 16 MiB static scratch refused before any device call
+    na = abi.LIB.rc_maps_from_logits_noalloc
+    assert abi.RC_STATIC_SCRATCH_BYTES == 16 << 20
+    assert na(FAKE, 28, 16, 4096, 121, dp, 2, FAKE, None) == -8
+    assert na(None, 28, 16, 4096, 120, dp, 2, FAKE, None) == -1
+    assert na(FAKE, 28, 16, 4096, 120, C.cast(bad, C.POINTER(C.c_int32)), 2, FAKE, None) == -4
+    d8 = (C.c_int32 * 8)(*range(8))
+    d8p = C.cast(d8, C.POINTER(C.c_int32))
+    assert 33 * 16384 * 8 * 4 > abi.RC_STATIC_SCRATCH_BYTES >= 32 * 16384 * 8 * 4
+    assert na(FAKE, 33, 16, 16384, 120, d8p, 8, FAKE, None) == -5
+    if NO_GPU:
+        assert na(FAKE, 28, 16, 16384, 120, d8p, 8, FAKE, None) == -6
 
 
 def test_text_and_update_validation(ctx):
