@@ -57,3 +57,50 @@ def download_slot(cache, t, L, B):
     V = np.stack([np.stack([to_np(cache.V(b, t, l)) for b in range(B)]) for l in range(L)])
     H = np.stack([np.stack([to_np(cache.H(b, t, l)) for b in range(B)]) for l in range(L)])
     return dict(K=K, V=V, H=H)
+
+
+def teacher_forced_reuse(shape, W, latent_b, t, tkv_o, idx, cache_b, got_b):
+    """Per-block parity of a region-reuse step with re-synchronised inputs.
+
+    Block l of the oracle takes as input the GPU's own output rows of block
+    l-1 (its H slot at the active tokens; block 0 takes the oracle's
+    embedding), so an error in one block does not compound through the
+    later ones.  cache_b: the slot the step started from (K, V [L,H,N,D], H
+    [L,N,C]); got_b: the slot the GPU left (same layout).  Returns the worst
+    normwise errors over blocks of the active rows' block output H, their
+    per-block change H_l - H_{l-1} (which a broken attention or gate moves by
+    O(1) under the stress weights, even where H itself is dominated by the
+    residual stream), and their keys and values."""
+    idx = np.asarray(idx, dtype=np.int64)
+    t0 = O.adaln_single(W, O.timestep_embedding(W, t))
+    X_in = O.patch_embed(W, latent_b, shape.grid_h, shape.grid_w, shape.patch)[idx]
+    worst = dict(H=0.0, dH=0.0, K=0.0, V=0.0)
+    for l, lw in enumerate(W["layers"]):
+        mod = O.layer_modulation(lw, t0)
+        X, K, V, _, _ = O.block_reuse(lw, X_in, idx, mod, tkv_o[l][0], tkv_o[l][1], cache_b["K"][l], cache_b["V"][l],
+                                      cache_b["H"][l], shape.heads)
+        gH = np.asarray(got_b["H"][l][idx], np.float64)
+        worst["H"] = max(worst["H"], relerr(gH, X))
+        worst["dH"] = max(worst["dH"], relerr(gH - X_in, X - X_in))
+        worst["K"] = max(worst["K"], relerr(got_b["K"][l][:, idx], K[:, idx]))
+        worst["V"] = max(worst["V"], relerr(got_b["V"][l][:, idx], V[:, idx]))
+        X_in = gH
+    return worst
+
+
+def teacher_forced_dense(shape, W, latent_b, t, tkv_o, got_b):
+    """teacher_forced_reuse for a dense step: every token, blocks fed the
+    GPU's previous block output (all N rows)."""
+    t0 = O.adaln_single(W, O.timestep_embedding(W, t))
+    X_in = O.patch_embed(W, latent_b, shape.grid_h, shape.grid_w, shape.patch)
+    worst = dict(H=0.0, dH=0.0, K=0.0, V=0.0)
+    for l, lw in enumerate(W["layers"]):
+        mod = O.layer_modulation(lw, t0)
+        X, K, V, _ = O.block_dense(lw, X_in, mod, tkv_o[l][0], tkv_o[l][1], shape.heads)
+        gH = np.asarray(got_b["H"][l], np.float64)
+        worst["H"] = max(worst["H"], relerr(gH, X))
+        worst["dH"] = max(worst["dH"], relerr(gH - X_in, X - X_in))
+        worst["K"] = max(worst["K"], relerr(got_b["K"][l], K))
+        worst["V"] = max(worst["V"], relerr(got_b["V"][l], V))
+        X_in = gH
+    return worst

@@ -165,6 +165,38 @@ def test_pos_embed_structure():
     assert abs(P2[5 * 2 + 1, 32] - math.sin(2.0)) < 1e-15
 
 
+def test_pos_embed_matches_library_routine():
+    """The position table equals an independent library implementation of
+    the 2-D sin-cos table (the OmDet-Turbo encoder's in transformers, float64):
+    frequency ladder, sin/cos order and which half holds which coordinate.
+    The library lists tokens column-major (x * gh + y); the oracle row-major
+    (y * gw + x).  Non-square grids, so swapping the coordinates fails."""
+    import torch
+    from transformers.models.omdet_turbo.modeling_omdet_turbo import OmDetTurboHybridEncoder as Enc
+    for gh, gw, C in ((5, 7, 64), (3, 11, 1152), (32, 32, 1152)):
+        lib = Enc.build_2d_sincos_position_embedding(gw, gh, C, 10000.0, dtype=torch.float64)[0].numpy()
+        P = O.pos_embed_2d(gh, gw, C)
+        ys, xs = np.divmod(np.arange(gh * gw), gw)
+        assert np.abs(P - lib[xs * gh + ys]).max() < 1e-12, (gh, gw, C)
+
+
+def test_pos_embed_frequency_ladder():
+    """Frequencies read back from the table (atan2 of the sin and cos columns
+    at x = 1, unambiguous since every frequency is <= 1 < pi) form the
+    geometric ladder from 1 down to 10^-4 * 10^(4/q) over q = C/4 columns."""
+    C = 1152
+    q = C // 4
+    P = O.pos_embed_2d(2, 3, C)
+    w = np.arctan2(P[1, :q], P[1, q:2 * q])  # token (y=0, x=1)
+    assert abs(w[0] - 1.0) < 1e-14
+    ratio = w[1:] / w[:-1]
+    assert np.abs(ratio - ratio[0]).max() < 1e-12
+    assert abs(w[-1] * 1e4 - 1e4 ** (1.0 / q)) < 1e-9
+    # the row half carries the same ladder in y: token (y=1, x=0)
+    wy = np.arctan2(P[3, C // 2:C // 2 + q], P[3, C // 2 + q:])
+    assert np.abs(wy - w).max() < 1e-14
+
+
 def test_alphas_cumprod_and_ddim_roundtrip():
     ac = O.alphas_cumprod()
     betas = np.linspace(1e-4, 0.02, 1000)
