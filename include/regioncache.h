@@ -8,8 +8,9 @@
  * localises the edit region from cross-attention maps.
  *
  * Paper passages the calls implement (RegionCache, arxiv 2608.29809):
- *   build cache      -- Sec. 3.2, "Hidden-State-Oriented Caching": a cache pool
- *                       of hidden states along the diffusion trajectory.
+ *   build cache      -- Sec. 3.2, "Hidden-State-Oriented Caching": per-step,
+ *                       per-block keys, values and block outputs of every token
+ *                       of a turn, kept for the next turn to reuse.
  *   localize region  -- Sec. 3.2: the edit region is the set of image tokens
  *                       whose aggregated cross-attention to a new or modified
  *                       text token reaches a threshold derived from that map.
@@ -146,10 +147,12 @@ typedef struct {
 
 /* Active token set (device arrays + host copy of the offsets).  Tokens of
  * chain b are idx[offsets[b] .. offsets[b+1]-1], chain-local and strictly
- * ascending.  Ascending order and uniqueness are the caller's promise; the
- * library does not re-check them on the device (out-of-range tokens would be
- * written out of their slot), rc_localize_region and rc_compact_mask produce
- * valid sets. */
+ * ascending.  The host checks only the per-chain counts (offsets_host);
+ * ascending order, range and agreement of the device offsets with
+ * offsets_host are the caller's promise unless it asks for the device check
+ * (rc_validate_active, or RC_VALIDATE on rc_reuse_step): without it an
+ * out-of-range token is written outside its slot.  rc_localize_region and
+ * rc_compact_mask produce valid sets. */
 typedef struct {
   const int32_t *idx;          /* device [offsets[batch]] */
   const int32_t *offsets;      /* device [batch+1] */
@@ -243,6 +246,10 @@ rc_status rc_build_cache(rc_ctx *ctx, const rc_cache_view *cache, int32_t step, 
 
 /* Flags of rc_reuse_step. */
 #define RC_FUSE_UPDATE 1u /* write active hidden rows straight into the slot's H */
+#define RC_VALIDATE 2u    /* check the active set on the device first (as rc_validate_active,
+                             with the first 16 bytes of the workspace as scratch): an invalid
+                             set returns RC_ERR_INDEX before any of the step's launches.
+                             Synchronises the stream. */
 
 /* RUN REUSE STEP (Sec. 3.3, 3.4): region-sparse step `step` over the active
  * set.  Per block, fresh keys/values of active tokens are written into the
@@ -262,6 +269,16 @@ rc_status rc_reuse_step(rc_ctx *ctx, const rc_cache_view *cache, int32_t step,
  * H arrays of slot `step` at the active tokens. */
 rc_status rc_update_cache(rc_ctx *ctx, const rc_cache_view *cache, int32_t step,
                           const rc_active_set *active, const void *active_hidden, void *stream);
+
+/* Device check of an active set (the active token set of Sec. 3.3) for a
+ * pool of `batch` chains: the host counts as in rc_reuse_step, then the
+ * device offsets must equal offsets_host and every chain's tokens must be
+ * strictly ascending (hence unique) and inside [0, N).  Returns RC_OK, or
+ * RC_ERR_INDEX with the first offending chain, entry and token in
+ * rc_last_error().  scratch: >= 16 bytes of caller device memory (overwritten).
+ * Reads the active set only, writes nothing else, synchronises the stream. */
+rc_status rc_validate_active(const rc_ctx *ctx, const rc_active_set *active, int32_t batch, void *scratch,
+                             size_t scratch_bytes, void *stream);
 
 /* HOST-RESIDENT POOL (Sec. 3.4, pipelined execution).  The cache pool may
  * live in pinned host memory (hipHostMalloc or torch pin_memory: page-locked

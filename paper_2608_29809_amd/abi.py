@@ -19,6 +19,7 @@ STATUS = {0: "RC_OK", -1: "RC_ERR_INVALID_ARG", -2: "RC_ERR_SHAPE", -3: "RC_ERR_
           -8: "RC_ERR_UNSUPPORTED"}
 RC_F32, RC_BF16 = 0, 1
 RC_FUSE_UPDATE = 1
+RC_VALIDATE = 2
 RC_STATIC_SCRATCH_BYTES = 16 << 20
 (RC_KC_GEMM, RC_KC_ATTN_SELF, RC_KC_ATTN_CROSS, RC_KC_ATTN_COMBINE, RC_KC_NORM, RC_KC_EMBED,
  RC_KC_FINAL, RC_KC_COND, RC_KC_MISC, RC_KC_GEMM_QKV, RC_KC_GEMM_FC1, RC_KC_GEMM_FC2, RC_KC_GEMM_PROJ,
@@ -97,6 +98,7 @@ def _load():
         "rc_reuse_step": (C.c_int, [P, C.POINTER(rc_cache_view), I32, C.POINTER(rc_active_set),
                                     C.POINTER(rc_step_io), P, U32, P, S, P]),
         "rc_update_cache": (C.c_int, [P, C.POINTER(rc_cache_view), I32, C.POINTER(rc_active_set), P, P]),
+        "rc_validate_active": (C.c_int, [P, C.POINTER(rc_active_set), I32, P, S, P]),
         "rc_staging_bytes": (S, [P, I32]),
         "rc_reuse_step_hosted": (C.c_int, [P, C.POINTER(rc_cache_view), I32, C.POINTER(rc_active_set),
                                            C.POINTER(rc_step_io), P, S, P, S, P]),
@@ -143,7 +145,7 @@ def _wrap(name):
 
 
 for _n in ["rc_create", "rc_cache_offsets", "rc_cache_latent_offset", "rc_prepare_text", "rc_build_cache",
-           "rc_reuse_step", "rc_update_cache", "rc_reuse_step_hosted", "rc_build_cache_hosted",
+           "rc_reuse_step", "rc_update_cache", "rc_validate_active", "rc_reuse_step_hosted", "rc_build_cache_hosted",
            "rc_localize_region", "rc_maps_from_logits", "rc_maps_from_logits_noalloc", "rc_compact_mask", "rc_sync", "rc_set_kernel_timing",
            "rc_get_kernel_timing"]:
     globals()[_n] = _wrap(_n)

@@ -866,6 +866,36 @@ static rc_status check_active(const rc_ctx *c, const rc_cache_view *cache, const
   return RC_OK;
 }
 
+// Device check of an active set whose host-side counts check_active has
+// accepted: the device offsets equal the host copy, and every chain's
+// tokens are strictly ascending and inside [0, N).  verdict_dev: 4 bytes of
+// device scratch.  Synchronises the stream; launches nothing else.
+static rc_status validate_active(const rc_ctx *c, const rc_active_set *a, int *verdict_dev, hipStream_t s) {
+  const int B = a->batch, total = a->offsets_host[B];
+  if (total == 0) return RC_OK;
+  std::vector<int> offs(B + 1);
+  RC_HIP(hipMemcpyAsync(offs.data(), a->offsets, sizeof(int) * (B + 1), hipMemcpyDeviceToHost, s));
+  RC_HIP(hipStreamSynchronize(s));
+  for (int b = 0; b <= B; ++b)
+    RC_CHECK(offs[b] == a->offsets_host[b], RC_ERR_INDEX, "device offsets[%d] = %d differs from offsets_host[%d] = %d",
+             b, offs[b], b, a->offsets_host[b]);
+  RC_HIP(rc::launch_validate_active(a->offsets, a->idx, B, c->N, verdict_dev, s));
+  int v = -1;
+  RC_HIP(hipMemcpyAsync(&v, verdict_dev, sizeof(int), hipMemcpyDeviceToHost, s));
+  RC_HIP(hipStreamSynchronize(s));
+  if (v < 0) return RC_OK;
+  const int b = (int)(std::upper_bound(offs.begin(), offs.end(), v) - offs.begin()) - 1;
+  int tok[2] = {0, 0};
+  const bool first = v == offs[b];
+  RC_HIP(hipMemcpyAsync(tok, a->idx + (first ? v : v - 1), sizeof(int) * (first ? 1 : 2), hipMemcpyDeviceToHost, s));
+  RC_HIP(hipStreamSynchronize(s));
+  if (first)
+    return fail(RC_ERR_INDEX, "active set: chain %d, entry %d: token %d outside [0, %d)", b, v - offs[b], tok[0],
+                c->N);
+  return fail(RC_ERR_INDEX, "active set: chain %d, entry %d: token %d after %d (not strictly ascending in [0, %d))", b,
+              v - offs[b], tok[1], tok[0], c->N);
+}
+
 rc_status rc_reuse_step(rc_ctx *c, const rc_cache_view *cache, int32_t step, const rc_active_set *active,
                         const rc_step_io *io, void *active_hidden, uint32_t flags, void *ws, size_t ws_bytes,
                         void *stream) {
@@ -875,10 +905,13 @@ rc_status rc_reuse_step(rc_ctx *c, const rc_cache_view *cache, int32_t step, con
   RC_TRY(check_io(c, io));
   RC_TRY(check_active(c, cache, active));
   RC_TRY(check_guided(io, cache->batch, active));
-  RC_CHECK((flags & ~RC_FUSE_UPDATE) == 0, RC_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
+  RC_CHECK((flags & ~(RC_FUSE_UPDATE | RC_VALIDATE)) == 0, RC_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
+  if (flags & RC_VALIDATE)
+    RC_CHECK(ws && aligned16(ws) && ws_bytes >= 16, RC_ERR_INVALID_ARG, "RC_VALIDATE needs the workspace");
   RC_CHECK(device_present(), RC_ERR_NO_DEVICE, "no HIP device");
   hipStream_t s = (hipStream_t)stream;
   const bool fuse = (flags & RC_FUSE_UPDATE) != 0;
+  if (flags & RC_VALIDATE) RC_TRY(validate_active(c, active, (int *)ws, s));
   return c->esz == 2 ? run_step<bf16>(c, cache, step, io, false, active, active_hidden, fuse, ws, ws_bytes, s)
                      : run_step<float>(c, cache, step, io, false, active, active_hidden, fuse, ws, ws_bytes, s);
 }
@@ -907,6 +940,20 @@ rc_status rc_update_cache(rc_ctx *c, const rc_cache_view *cache, int32_t step, c
     }));
   }
   return RC_OK;
+}
+
+rc_status rc_validate_active(const rc_ctx *c, const rc_active_set *active, int32_t batch, void *scratch,
+                             size_t scratch_bytes, void *stream) {
+  g_err.clear();
+  RC_CHECK(c && active, RC_ERR_INVALID_ARG, "null argument to rc_validate_active");
+  RC_CHECK(batch >= 1 && batch <= 32767, RC_ERR_SHAPE, "batch %d out of range", batch);
+  rc_cache_view v{};
+  v.batch = batch;
+  RC_TRY(check_active(c, &v, active));
+  RC_CHECK(scratch && aligned16(scratch) && scratch_bytes >= 16, RC_ERR_INVALID_ARG,
+           "scratch must be >= 16 bytes of 16-byte aligned device memory");
+  RC_CHECK(device_present(), RC_ERR_NO_DEVICE, "no HIP device");
+  return validate_active(c, active, (int *)scratch, (hipStream_t)stream);
 }
 
 size_t rc_staging_bytes(const rc_ctx *c, int32_t batch) {

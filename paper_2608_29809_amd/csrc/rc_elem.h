@@ -70,5 +70,7 @@ hipError_t launch_sum_partials(const float *partial, int n_parts, int n, float *
 hipError_t launch_localize(const float *maps, int B, int gh, int gw, int n_delta, float threshold, int radius,
                            uint8_t *mask, hipStream_t s);
 hipError_t launch_compact(const uint8_t *mask, int B, int N, int *idx, int *offsets, hipStream_t s);
+// verdict[0] = first invalid position of an active set, or -1 (offsets must be valid).
+hipError_t launch_validate_active(const int *offsets, const int *idx, int B, int N, int *verdict, hipStream_t s);
 
 }  // namespace rc

@@ -6,6 +6,8 @@
 #include "rc_launch.h"
 #include "rc_elem.h"
 
+#include <climits>
+
 namespace rc {
 
 constexpr int LG_TOK = 64;  // tokens per workgroup, 16 per wave
@@ -205,6 +207,41 @@ __global__ __launch_bounds__(1024) void compact_kernel(const uint8_t *mask, int 
     }
   }
   if (tid == 0) offsets[B] = base;
+}
+
+// Validity of an active set (device offsets already checked equal to the
+// host copy, so every chain's range lies inside idx[0, total)): the first
+// position p, in index order, whose token is outside [0, N) or not larger
+// than the token before it in the same chain; -1 if there is none.  One
+// workgroup; each thread keeps its smallest bad position, then a fixed-order
+// reduction; thread 0 writes the verdict.
+__global__ __launch_bounds__(1024) void validate_active_kernel(const int *offsets, const int *idx, int B, int N,
+                                                               int *verdict) {
+  __shared__ int red[16];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int bad = INT_MAX;
+  for (int b = 0; b < B; ++b) {
+    const int lo = offsets[b], hi = offsets[b + 1];
+    for (int i = lo + tid; i < hi; i += 1024) {
+      const int v = idx[i];
+      const bool ok = v >= 0 && v < N && (i == lo || idx[i - 1] < v);
+      if (!ok) bad = min(bad, i);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) bad = min(bad, __shfl_xor(bad, o, 64));
+  if (lane == 0) red[wave] = bad;
+  __syncthreads();
+  if (tid == 0) {
+    int m = red[0];
+    for (int w = 1; w < 16; ++w) m = min(m, red[w]);
+    verdict[0] = m == INT_MAX ? -1 : m;
+  }
+}
+
+hipError_t launch_validate_active(const int *offsets, const int *idx, int B, int N, int *verdict, hipStream_t s) {
+  rc_launch(validate_active_kernel, dim3(1), dim3(1024), 0, s, offsets, idx, B, N, verdict);
+  return hipGetLastError();
 }
 
 hipError_t launch_compact(const uint8_t *mask, int B, int N, int *idx, int *offsets, hipStream_t s) {

@@ -219,7 +219,9 @@ class RegionCacheModel:
     def reuse_step(self, cache: CacheBuffer, step: int, act: ActiveSet, inp: torch.Tensor, timestep: int,
                    timestep_next: int, tkv: torch.Tensor, delta=None, maps=None, latent_out=None, t_vec=None,
                    fuse: bool = True, active_hidden: Optional[torch.Tensor] = None, text_valid=None,
-                   guidance=None):
+                   guidance=None, validate: bool = False):
+        """validate: check the active set on the device first (RC_VALIDATE);
+        an invalid set raises RcError (RC_ERR_INDEX) before any launch."""
         io, keep = self._io(inp, timestep, timestep_next, tkv, delta, maps, latent_out, t_vec, text_valid,
                             guidance)
         ws = self.workspace(max(act.total, 1), cache.batch)
@@ -231,8 +233,17 @@ class RegionCacheModel:
             abi.rc_reuse_step_hosted(self.ctx, C.byref(cache.view), step, C.byref(s), C.byref(io), _ptr(st),
                                      st.numel(), _ptr(ws), ws.numel(), _stream())
         else:
+            flags = (abi.RC_FUSE_UPDATE if fuse else 0) | (abi.RC_VALIDATE if validate else 0)
             abi.rc_reuse_step(self.ctx, C.byref(cache.view), step, C.byref(s), C.byref(io), _ptr(active_hidden),
-                              abi.RC_FUSE_UPDATE if fuse else 0, _ptr(ws), ws.numel(), _stream())
+                              flags, _ptr(ws), ws.numel(), _stream())
+
+    def validate_active(self, act: ActiveSet):
+        """Device check of an active set (rc_validate_active); raises RcError
+        with RC_ERR_INDEX if a chain's tokens are not strictly ascending in
+        [0, N) or the device offsets differ from the host copy."""
+        scratch = self.workspace(1, act.batch)
+        s = act.struct()
+        abi.rc_validate_active(self.ctx, C.byref(s), act.batch, _ptr(scratch), scratch.numel(), _stream())
 
     def update_cache(self, cache: CacheBuffer, step: int, act: ActiveSet, active_hidden: torch.Tensor):
         s = act.struct()

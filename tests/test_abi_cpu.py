@@ -151,8 +151,38 @@ def test_reuse_validation(ctx):
     assert step(ctx, C.byref(view), 1, C.byref(a), C.byref(_io()), None, 1, FAKE, ws, None) == -2
     a, k5 = aset([0, 10, 20])
     assert step(ctx, C.byref(view), 1, C.byref(a), C.byref(_io()), None, 4, FAKE, ws, None) == -1  # flags
+    # RC_VALIDATE is a known flag; it needs the workspace for its verdict
+    fv = abi.RC_FUSE_UPDATE | abi.RC_VALIDATE
+    assert step(ctx, C.byref(view), 1, C.byref(a), C.byref(_io()), None, fv, None, ws, None) == -1
+    assert step(ctx, C.byref(view), 1, C.byref(a), C.byref(_io()), None, fv, FAKE, 8, None) == -1
     if NO_GPU:
         assert step(ctx, C.byref(view), 1, C.byref(a), C.byref(_io()), None, 1, FAKE, ws, None) == -6
+        assert step(ctx, C.byref(view), 1, C.byref(a), C.byref(_io()), None, fv, FAKE, ws, None) == -6
+
+
+def test_validate_active_plumbing(ctx):
+    """rc_validate_active: host-side counts checked first (as for a step),
+    then the scratch, then the device."""
+    val = abi.LIB.rc_validate_active
+
+    def aset(offs, batch=2):
+        h = (C.c_int32 * len(offs))(*offs)
+        return abi.rc_active_set(FAKE, FAKE, C.cast(h, C.POINTER(C.c_int32)), batch), h
+
+    a, k = aset([0, 10, 20])
+    assert val(None, C.byref(a), 2, FAKE, 16, None) == -1
+    assert val(ctx, None, 2, FAKE, 16, None) == -1
+    assert val(ctx, C.byref(a), 3, FAKE, 16, None) == -2        # batch differs from the set's
+    assert val(ctx, C.byref(a), 0, FAKE, 16, None) == -2
+    b, k2 = aset([0, 10, 5])
+    assert val(ctx, C.byref(b), 2, FAKE, 16, None) == -4        # not monotone on the host
+    b, k3 = aset([0, 2000, 2001])
+    assert val(ctx, C.byref(b), 2, FAKE, 16, None) == -4        # more tokens than the grid
+    assert val(ctx, C.byref(a), 2, None, 16, None) == -1
+    assert val(ctx, C.byref(a), 2, FAKE, 8, None) == -1
+    assert val(ctx, C.byref(a), 2, FAKE + 4, 16, None) == -1
+    if NO_GPU:
+        assert val(ctx, C.byref(a), 2, FAKE, 16, None) == -6
 
 
 def test_guidance_validation(ctx):
