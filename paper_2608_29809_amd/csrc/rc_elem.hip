@@ -25,14 +25,14 @@ hipError_t launch_build_rows(const int *offsets, const int *idx, int B, int R, i
   return hipGetLastError();
 }
 
-// Dense-step offsets: offsets[b] = b*N.
+// Dense-step offsets: offsets[b] = b*N for b = 0..B (B+1 entries, any B).
 __global__ void dense_offsets_kernel(int *offsets, int B, int N) {
-  const int b = threadIdx.x;
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b <= B) offsets[b] = b * N;
 }
 
 hipError_t launch_dense_offsets(int *offsets, int B, int N, hipStream_t s) {
-  rc_launch(dense_offsets_kernel, dim3(1), dim3(256), 0, s, offsets, B, N);
+  rc_launch(dense_offsets_kernel, dim3((B + 1 + 255) / 256), dim3(256), 0, s, offsets, B, N);
   return hipGetLastError();
 }
 

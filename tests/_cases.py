@@ -59,6 +59,36 @@ def download_slot(cache, t, L, B):
     return dict(K=K, V=V, H=H)
 
 
+BF16_U = 2.0 ** -8  # unit roundoff of bf16 storage (8 significant bits, round to nearest)
+
+
+def _block_errors(gH, X, X_in, gK, K, gV, V, storage_u):
+    """Errors of one block: normwise H, K, V, and the per-block change
+    dH = H_l - H_(l-1) with its measurement floor.  Both ends of the GPU's
+    change are storage-rounded block outputs (the GPU's own block input was
+    unrounded), so |dH_gpu - dH_true| carries up to u (|H_l| + |H_(l-1)|) of
+    rounding that no kernel can remove; dH_floor is that bound relative to
+    max |dH|."""
+    d_ref = X - X_in
+    return dict(H=relerr(gH, X), dH=relerr(gH - X_in, d_ref), K=relerr(gK, K), V=relerr(gV, V),
+                dH_floor=storage_u * (np.abs(gH).max() + np.abs(X_in).max()) / max(np.abs(d_ref).max(), 1e-30))
+
+
+def gate_failures(per_block, tl):
+    """Blocks failing the per-block gate: H, K and V within `tl`, the
+    per-block change within `tl` plus its storage-rounding floor."""
+    bad = []
+    for l, e in enumerate(per_block):
+        if not (e["H"] < tl and e["K"] < tl and e["V"] < tl and e["dH"] < tl + e["dH_floor"]):
+            bad.append((l, e))
+    return bad
+
+
+def summarize(per_block):
+    """Worst value of each error over the blocks."""
+    return {k: max(e[k] for e in per_block) for k in ("H", "dH", "K", "V", "dH_floor")}
+
+
 def teacher_forced_reuse(shape, W, latent_b, t, tkv_o, idx, cache_b, got_b):
     """Per-block parity of a region-reuse step with re-synchronised inputs.
 
@@ -66,41 +96,38 @@ def teacher_forced_reuse(shape, W, latent_b, t, tkv_o, idx, cache_b, got_b):
     l-1 (its H slot at the active tokens; block 0 takes the oracle's
     embedding), so an error in one block does not compound through the
     later ones.  cache_b: the slot the step started from (K, V [L,H,N,D], H
-    [L,N,C]); got_b: the slot the GPU left (same layout).  Returns the worst
-    normwise errors over blocks of the active rows' block output H, their
-    per-block change H_l - H_{l-1} (which a broken attention or gate moves by
-    O(1) under the stress weights, even where H itself is dominated by the
-    residual stream), and their keys and values."""
+    [L,N,C]); got_b: the slot the GPU left (same layout).  Returns, per
+    block, the normwise errors of the active rows' block output H, their
+    per-block change H_l - H_(l-1) (which a broken attention or gate moves
+    by O(1) under the stress weights, even where H itself is dominated by the
+    residual stream) with its storage floor, and their keys and values."""
     idx = np.asarray(idx, dtype=np.int64)
+    u = BF16_U if shape.dtype == "bf16" else 2.0 ** -24
     t0 = O.adaln_single(W, O.timestep_embedding(W, t))
     X_in = O.patch_embed(W, latent_b, shape.grid_h, shape.grid_w, shape.patch)[idx]
-    worst = dict(H=0.0, dH=0.0, K=0.0, V=0.0)
+    out = []
     for l, lw in enumerate(W["layers"]):
         mod = O.layer_modulation(lw, t0)
         X, K, V, _, _ = O.block_reuse(lw, X_in, idx, mod, tkv_o[l][0], tkv_o[l][1], cache_b["K"][l], cache_b["V"][l],
                                       cache_b["H"][l], shape.heads)
         gH = np.asarray(got_b["H"][l][idx], np.float64)
-        worst["H"] = max(worst["H"], relerr(gH, X))
-        worst["dH"] = max(worst["dH"], relerr(gH - X_in, X - X_in))
-        worst["K"] = max(worst["K"], relerr(got_b["K"][l][:, idx], K[:, idx]))
-        worst["V"] = max(worst["V"], relerr(got_b["V"][l][:, idx], V[:, idx]))
+        out.append(_block_errors(gH, X, X_in, got_b["K"][l][:, idx], K[:, idx], got_b["V"][l][:, idx], V[:, idx],
+                                 u if l > 0 else u / 2))
         X_in = gH
-    return worst
+    return out
 
 
 def teacher_forced_dense(shape, W, latent_b, t, tkv_o, got_b):
     """teacher_forced_reuse for a dense step: every token, blocks fed the
     GPU's previous block output (all N rows)."""
+    u = BF16_U if shape.dtype == "bf16" else 2.0 ** -24
     t0 = O.adaln_single(W, O.timestep_embedding(W, t))
     X_in = O.patch_embed(W, latent_b, shape.grid_h, shape.grid_w, shape.patch)
-    worst = dict(H=0.0, dH=0.0, K=0.0, V=0.0)
+    out = []
     for l, lw in enumerate(W["layers"]):
         mod = O.layer_modulation(lw, t0)
         X, K, V, _ = O.block_dense(lw, X_in, mod, tkv_o[l][0], tkv_o[l][1], shape.heads)
         gH = np.asarray(got_b["H"][l], np.float64)
-        worst["H"] = max(worst["H"], relerr(gH, X))
-        worst["dH"] = max(worst["dH"], relerr(gH - X_in, X - X_in))
-        worst["K"] = max(worst["K"], relerr(got_b["K"][l], K))
-        worst["V"] = max(worst["V"], relerr(got_b["V"][l], V))
+        out.append(_block_errors(gH, X, X_in, got_b["K"][l], K, got_b["V"][l], V, u if l > 0 else u / 2))
         X_in = gH
-    return worst
+    return out

@@ -13,7 +13,8 @@ import torch
 
 import oracle as O
 import synth
-from _cases import download_slot, oracle_text_kv, relerr, to_np, tol, upload_slot, weights
+from _cases import (download_slot, gate_failures, oracle_text_kv, relerr, summarize, teacher_forced_dense,
+                    teacher_forced_reuse, to_np, tol, upload_slot, weights)
 
 pytestmark = pytest.mark.gpu
 
@@ -182,13 +183,36 @@ def _reuse_case(shape, seed, per_chain_idx, t=500, t_next=450, stress=False, del
     got["latent_next"] = to_np(lat_out)
     got["maps"] = to_np(maps)
     got["traj_next"] = np.stack([to_np(cache.latent(b, step + 1)) for b in range(B)])
-    refs = []
+    refs, tkvs = [], []
     for b in range(B):
         tkv_o = oracle_text_kv(shape, W, txt[b])
+        tkvs.append(tkv_o)
         cs = dict(K=slot["K"][:, b], V=slot["V"][:, b], H=slot["H"][:, b])
         refs.append(O.reuse_step(shape, W, lat[b], t, t_next, tkv_o, per_chain_idx[b], cs, lat_next_cached[b],
                                  np.array(delta)))
-    return got, refs, dict(slot=slot, lat_next_cached=lat_next_cached, model=model, cache=cache, W=W)
+    return got, refs, dict(slot=slot, lat_next_cached=lat_next_cached, model=model, cache=cache, W=W, lat=lat,
+                           tkv_o=tkvs, t=t)
+
+
+def _check_teacher_forced(shape, got, per_chain_idx, ctx):
+    """Per-block gate with re-synchronised inputs (tests/_cases.py): each
+    block of the oracle is fed the GPU's previous block output; block
+    outputs, keys and values of the active rows within the bf16 tolerance in
+    every block, and their per-block change within it plus the rounding
+    floor of its measurement from the storage-rounded block outputs."""
+    tl = tol(shape)
+    for b, idx in enumerate(per_chain_idx):
+        idx = np.asarray(idx)
+        if idx.size == 0:
+            continue
+        cache_b = {k: ctx["slot"][k][:, b] for k in ("K", "V", "H")}
+        got_b = {k: got[k][:, b] for k in ("K", "V", "H")}
+        per = teacher_forced_reuse(shape, ctx["W"], ctx["lat"][b], ctx["t"], ctx["tkv_o"][b], idx, cache_b, got_b)
+        w = summarize(per)
+        _say(f"chain {b} R={idx.size} per block (re-synchronised), worst: " +
+             " ".join(f"{k} {v:.2e}" for k, v in w.items()))
+        bad = gate_failures(per, tl)
+        assert not bad, (b, bad[:3])
 
 
 def _check_reuse(shape, got, refs, per_chain_idx, ctx, tolerance=None):
@@ -218,13 +242,35 @@ def _check_reuse(shape, got, refs, per_chain_idx, ctx, tolerance=None):
 
 
 @pytest.mark.timeout(300)
-def test_c2_reuse_step_full_model():
-    """512 px, 28 blocks, bf16, t = 500, a 15 % rectangle (11 x 14 tokens)."""
-    _say("c2 reuse full")
+@pytest.mark.parametrize("stress", [False, True])
+def test_c2_reuse_step_full_model(stress):
+    """512 px, 28 blocks, bf16, t = 500, a 15 % rectangle (11 x 14 tokens).
+    With the stress weights (every branch moves the state by O(1)) each
+    block is also gated with re-synchronised inputs."""
+    _say("c2 reuse full, stress", stress)
     s = synth.shape_c2()
     idx = np.flatnonzero(synth.rect_mask(s.grid_h, s.grid_w, 11, 14, 9, 5))
-    got, refs, ctx = _reuse_case(s, 0, [idx])
-    _check_reuse(s, got, refs, [idx], ctx)
+    got, refs, ctx = _reuse_case(s, 0, [idx], stress=stress)
+    if stress:
+        _check_teacher_forced(s, got, [idx], ctx)
+        _report_free_running(s, got, refs, [idx])
+    else:
+        _check_reuse(s, got, refs, [idx], ctx)
+
+
+def _report_free_running(shape, got, refs, per_chain_idx):
+    """Errors of the whole step against the free-running oracle (each side
+    feeding its own blocks through all blocks), beside the per-block gate:
+    within 2e-2 as well."""
+    for b, r in enumerate(refs):
+        idx = np.asarray(per_chain_idx[b])
+        if idx.size == 0:
+            continue
+        e = dict(H=relerr(got["H"][:, b][:, idx], r["H"][:, idx]),
+                 K=relerr(got["K"][:, b][:, :, idx], r["K"][:, :, idx]),
+                 latent=relerr(got["latent_next"][b], r["latent_next"]), maps=relerr(got["maps"][b], r["maps"]))
+        _say(f"chain {b} free-running whole step: " + " ".join(f"{k} {v:.2e}" for k, v in e.items()))
+        assert max(e.values()) < tol(shape), (b, e)
 
 
 @pytest.mark.parametrize("counts", [[1, 63, 0], [64, 65, 129], [127, 128, 1024]])
@@ -298,6 +344,33 @@ def test_dense_step_vs_oracle():
     assert torch.equal(out2, out) and torch.equal(maps2, maps)
 
 
+@pytest.mark.timeout(300)
+def test_dense_step_300_chains():
+    """A dense step of 300 chains (more than one 256-thread block of chain
+    offsets): one block on an 8 x 8 grid, 19200 rows.  Chains on both sides
+    of 256 match the oracle, so every chain's row range was set."""
+    _say("dense step, 300 chains")
+    s = synth.ModelShape(layers=1, grid_h=8, grid_w=8, text_dim=128, dtype="bf16")
+    B = 300
+    W = synth.make_weights(s, seed=16, stress=True)
+    txt = synth.make_text(s, B, 16)
+    lat = synth.make_latent(s, B, 16)
+    model = RegionCacheModel(s, W)
+    cache = model.alloc_cache(B, 1)
+    tkv = model.prepare_text(model.to_storage(txt))
+    out = torch.empty(lat.shape, device="cuda")
+    model.build_cache(cache, 0, torch.from_numpy(lat).cuda(), 600, 550, tkv, latent_out=out)
+    torch.cuda.synchronize()
+    o = to_np(out)
+    assert np.isfinite(o).all()
+    for b in (0, 1, 255, 256, 257, 299):
+        ref = O.dense_step(s, W, lat[b], 600, 550, oracle_text_kv(s, W, txt[b]))
+        e_h = relerr(to_np(cache.H(b, 0, 0)), ref["H"][0])
+        e_l = relerr(o[b], ref["latent_next"])
+        _say(f"chain {b}: H {e_h:.2e} latent {e_l:.2e}")
+        assert e_h < 2e-2 and e_l < 2e-2
+
+
 @pytest.mark.gpu
 @pytest.mark.timeout(300)
 def test_dense_step_two_chains():
@@ -333,7 +406,7 @@ def test_dense_step_full_grid():
     self-attention) against the oracle, maps included."""
     _say("dense step, 4096 tokens")
     s = synth.ModelShape(layers=2, grid_h=64, grid_w=64, dtype="bf16")
-    W = synth.make_weights(s, seed=9)
+    W = synth.make_weights(s, seed=9, stress=True)
     txt = synth.make_text(s, 1, 9)
     lat = synth.make_latent(s, 1, 9)
     model = RegionCacheModel(s, W)
@@ -353,6 +426,10 @@ def test_dense_step_full_grid():
     e_l, e_m = relerr(to_np(out)[0], ref["latent_next"]), relerr(to_np(maps)[0], ref["maps"])
     _say("latent", e_l, "maps", e_m)
     assert e_l < 2e-2 and e_m < 2e-2
+    per = teacher_forced_dense(s, W, lat[0], 950, oracle_text_kv(s, W, txt[0]),
+                               {k: got[k][:, 0] for k in ("K", "V", "H")})
+    _say("per block (re-synchronised), worst: " + " ".join(f"{k} {v:.2e}" for k, v in summarize(per).items()))
+    assert not gate_failures(per, 2e-2)
 
 
 @pytest.mark.gpu
@@ -368,8 +445,9 @@ def test_four_chains_mixed_fractions():
            for i, f in enumerate((0.05, 0.10, 0.25, 0.50))]
     _say("four chains", [p.size for p in per])
     assert sum(p.size for p in per) > 3072
-    got, refs, ctx = _reuse_case(s, 12, per, t=640, t_next=590)
+    got, refs, ctx = _reuse_case(s, 12, per, t=640, t_next=590, stress=True)
     _check_reuse(s, got, refs, per, ctx)
+    _check_teacher_forced(s, got, per, ctx)
 
 
 @pytest.mark.gpu
@@ -382,8 +460,9 @@ def test_fraction_sweep_workloads(frac):
     s = synth.ModelShape(layers=2, grid_h=64, grid_w=64, dtype="bf16")
     per = synth.sweep_regions(0, frac)
     _say("fraction sweep", frac, [p.size for p in per])
-    got, refs, ctx = _reuse_case(s, 13, per, t=700, t_next=650)
+    got, refs, ctx = _reuse_case(s, 13, per, t=700, t_next=650, stress=True)
     _check_reuse(s, got, refs, per, ctx)
+    _check_teacher_forced(s, got, per, ctx)
 
 
 @pytest.mark.gpu
@@ -484,6 +563,27 @@ def test_c3_reuse_step_full_size(region):
     _check_reuse(s, got, refs, [idx], ctx)
 
 
+@pytest.mark.timeout(600)
+def test_c3_reuse_step_full_size_stress():
+    """The benchmark's own 1024 px region (723 rows, 4096 keys per head, five
+    key splits plus the combine, 28 blocks) with the stress weights: every
+    block gated with re-synchronised inputs (block outputs, their per-block
+    change, keys and values of the active rows), so a wrong self-attention
+    in the launch configuration the benchmark times cannot hide behind the
+    residual stream."""
+    _say("c3 reuse full, stress, bench region")
+    s = synth.shape_c3()
+    idx = np.flatnonzero(synth.c3_edit_region(0)[0])
+    assert idx.size == 723
+    got, refs, ctx = _reuse_case(s, 0, [idx], t=842, t_next=789, stress=True)
+    _check_teacher_forced(s, got, [idx], ctx)
+    _report_free_running(s, got, refs, [idx])
+    # outside the region the slot is the cache, bit for bit
+    inact = np.setdiff1d(np.arange(s.tokens), idx)
+    assert np.array_equal(got["H"][:, 0][:, inact], ctx["slot"]["H"][:, 0][:, inact])
+    assert np.array_equal(got["K"][:, 0][:, :, inact], ctx["slot"]["K"][:, 0][:, :, inact])
+
+
 @pytest.mark.gpu
 @pytest.mark.timeout(400)
 @pytest.mark.parametrize("region", ["blob10", "bench15"])
@@ -498,8 +598,9 @@ def test_reuse_step_2048px(region):
         assert idx.size == 2458
     else:
         idx = np.flatnonzero(synth.blob_mask(128, 128, 0.10, 2, np.random.default_rng(3)))
-    got, refs, ctx = _reuse_case(s, 3, [idx], t=600, t_next=550)
+    got, refs, ctx = _reuse_case(s, 3, [idx], t=600, t_next=550, stress=True)
     _check_reuse(s, got, refs, [idx], ctx)
+    _check_teacher_forced(s, got, [idx], ctx)
 
 
 @pytest.mark.gpu
