@@ -27,7 +27,7 @@ import torch
 
 from .runtime import ActiveSet, CacheBuffer, RegionCacheModel, compact_mask
 
-__all__ = ["timestep_grid", "prompt_similarity", "reuse_cutoff", "step_plan", "EditSession"]
+__all__ = ["timestep_grid", "prompt_similarity", "delta_similarity", "reuse_cutoff", "step_plan", "EditSession"]
 
 
 def timestep_grid(T: int) -> np.ndarray:
@@ -62,12 +62,27 @@ def step_plan(T: int, rho: float = 0.2, reading: str = "dense_then_reuse", s: Op
     raise ValueError(f"unknown reading {reading!r}")
 
 
+def delta_similarity(txt_before: torch.Tensor, txt_after: torch.Tensor, delta_cols: Sequence[int]) -> List[float]:
+    """Eq. 1 per chain: cosine similarity of the edited tokens' embeddings
+    before and after the edit.  The embedding of the edited tokens is taken
+    to be the prompt features at the delta columns (the text features the
+    caption projection consumes), flattened over those columns.  Only these
+    few rows are copied to the host."""
+    cols = torch.as_tensor([int(c) for c in delta_cols], dtype=torch.long, device=txt_before.device)
+    a = txt_before.index_select(1, cols).float().cpu().numpy()
+    b = txt_after.index_select(1, cols).float().cpu().numpy()
+    return [prompt_similarity(a[i], b[i]) for i in range(a.shape[0])]
+
+
 class EditSession:
     """A batch of edit chains sharing one cache pool of T steps.
 
     ``first_turn`` generates from noise with T dense steps, which fills the
     pool; every ``edit_turn`` then runs the plan of its reading, keeping the
-    pool equal to the latest turn's trajectory."""
+    pool equal to the latest turn's trajectory.  Under the "paper" reading
+    each chain has its own reuse cutoff (Eq. 2 on its own Eq. 1 similarity):
+    at step s a chain is active ("reuse") once s >= its cutoff and keeps the
+    cache ("copy", no active token) before, all chains in one step call."""
 
     def __init__(self, model: RegionCacheModel, batch: int, T: int = 20, rho: float = 0.2, tau_s: float = 0.8,
                  reading: str = "dense_then_reuse", threshold: float = 0.3, radius: int = 1,
@@ -86,6 +101,7 @@ class EditSession:
         self.cache: CacheBuffer = model.alloc_cache(batch, T)
         self.tgrid = timestep_grid(T)
         self.turns = 0
+        self.prev_txt: Optional[torch.Tensor] = None
 
     def _t_next(self, s: int) -> int:
         return int(self.tgrid[s + 1]) if s + 1 < self.T else -1
@@ -102,33 +118,59 @@ class EditSession:
                           guidance=self.guidance)
             x = nxt
         self.turns = 1
+        self.prev_txt = txt
         return x
 
+    def _chain_lists(self, act: ActiveSet) -> List[np.ndarray]:
+        idx = act.idx[:max(act.total, 1)].cpu().numpy()[:act.total]
+        off = [int(v) for v in act.host]
+        return [idx[off[b]:off[b + 1]] for b in range(act.batch)]
+
     def edit_turn(self, txt: torch.Tensor, x_T: torch.Tensor, delta_cols: Sequence[int],
-                  similarity: Optional[float] = None, region: Optional[ActiveSet] = None) -> dict:
+                  similarity=None, region: Optional[ActiveSet] = None) -> dict:
         """One editing turn with the new prompt features txt and the same
         initial noise x_T.  delta_cols are the text positions of the new or
-        changed tokens; similarity is Eq. 1's s for the "paper" reading;
-        region overrides the localised active set (required by the "paper"
-        reading).  Returns the final latent, the plan, the active set and (for
+        changed tokens.  similarity is Eq. 1's s for the "paper" reading: a
+        number for every chain, one per chain, or None to compute it per
+        chain from the previous turn's and this turn's features at the delta
+        columns (delta_similarity).  region overrides the localised active
+        set (required by the "paper" reading, which runs no dense step).
+        Returns the final latent, chain 0's plan ("plan"), every chain's plan
+        ("plans"), the similarities, the active set and (for
         "dense_then_reuse") the localisation mask."""
         if self.turns == 0:
             raise RuntimeError("edit_turn needs a first turn to fill the cache pool")
         m = self.model
-        plan = step_plan(self.T, self.rho, self.reading, similarity, self.tau_s)
-        n_dense = plan.count("dense")
-        if region is None and n_dense == 0 and "reuse" in plan:
+        B = self.batch
+        sims: Optional[List[float]] = None
+        if self.reading == "paper":
+            if similarity is None:
+                sims = delta_similarity(self.prev_txt, txt, delta_cols)
+            elif np.ndim(similarity) == 0:
+                sims = [float(similarity)] * B
+            else:
+                sims = [float(v) for v in similarity]
+            if self.guidance is not None:  # both branches of an image follow the conditional one
+                sims = [sims[b - b % 2] for b in range(B)]
+            plans = [step_plan(self.T, self.rho, "paper", sims[b], self.tau_s) for b in range(B)]
+        else:
+            plans = [step_plan(self.T, self.rho, self.reading)] * B
+        n_dense = plans[0].count("dense")
+        if region is None and n_dense == 0 and any("reuse" in p for p in plans):
             raise ValueError("this plan has no dense step to localise the region from: pass region")
         tkv = m.prepare_text(txt)
         x = x_T.contiguous()
         act, mask = region, None
-        empty = ActiveSet.from_lists([np.zeros(0, np.int32)] * self.batch)
-        for s, what in enumerate(plan):
+        lists = self._chain_lists(region) if region is not None else None
+        empty = np.zeros(0, np.int32)
+        step_sets = {}
+        for s in range(self.T):
+            what = [p[s] for p in plans]
             nxt = torch.empty_like(x)
             t, tn = int(self.tgrid[s]), self._t_next(s)
-            if what == "dense":
+            if what[0] == "dense":
                 emit = region is None and s == n_dense - 1
-                maps = torch.zeros((self.batch, m.N, len(delta_cols)), device=x.device) if emit else None
+                maps = torch.zeros((B, m.N, len(delta_cols)), device=x.device) if emit else None
                 m.build_cache(self.cache, s, x, t, tn, tkv, list(delta_cols) if emit else None, maps, nxt,
                               guidance=self.guidance)
                 if emit:
@@ -136,10 +178,14 @@ class EditSession:
                     if self.guidance is not None:  # the conditional branch's region for both branches
                         mask = mask[0::2].repeat_interleave(2, dim=0).contiguous()
                         act = compact_mask(mask)
-            elif what == "copy":
-                m.reuse_step(self.cache, s, empty, x, t, tn, tkv, latent_out=nxt, guidance=self.guidance)
+                    lists = self._chain_lists(act)
             else:
-                m.reuse_step(self.cache, s, act, x, t, tn, tkv, latent_out=nxt, guidance=self.guidance)
+                key = tuple(w == "reuse" for w in what)
+                if key not in step_sets:
+                    step_sets[key] = ActiveSet.from_lists([lists[b] if key[b] else empty for b in range(B)]) \
+                        if any(key) else ActiveSet.from_lists([empty] * B)
+                m.reuse_step(self.cache, s, step_sets[key], x, t, tn, tkv, latent_out=nxt, guidance=self.guidance)
             x = nxt
         self.turns += 1
-        return dict(latent=x, plan=plan, active=act, mask=mask)
+        self.prev_txt = txt
+        return dict(latent=x, plan=plans[0], plans=plans, similarity=sims, active=act, mask=mask)

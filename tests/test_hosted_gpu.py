@@ -2,14 +2,18 @@
 a pool in pinned host memory and on a device pool of identical contents
 gives bit-identical results -- every slot of every block and chain, the
 latent, the trajectory and the maps -- for a region-reuse step and a dense
-step.  Five blocks, so the three-entry staging ring wraps around."""
+step, and both match the oracle (whole step within 2e-2, and every block
+with re-synchronised inputs).  Five blocks, so the three-entry staging ring
+wraps around; three ragged chains, one of them with no active token."""
 import numpy as np
 import pytest
 import torch
 
+import oracle as O
 import synth
 from paper_2608_29809_amd.runtime import ActiveSet, RegionCacheModel
-from _cases import download_slot, to_np, upload_slot, weights
+from _cases import (download_slot, gate_failures, oracle_text_kv, relerr, summarize, teacher_forced_dense,
+                    teacher_forced_reuse, to_np, upload_slot, weights)
 
 pytestmark = pytest.mark.gpu
 
@@ -71,6 +75,25 @@ def test_hosted_pool_matches_device_pool():
     before = synth.make_cache_slot(shape, B, 11)
     got = download_slot(host, 1, shape.layers, B)
     assert not np.array_equal(got["H"][:, 0][:, per[0]], before["H"][:, 0][:, per[0]])
+    # and the hosted step is the method's step: against the oracle
+    lat_np = to_np(lat)
+    lat_next = synth.make_latent(shape, B, 11, stream=77)
+    tkv_o = [oracle_text_kv(shape, W, txt[b]) for b in range(B)]
+    for b in range(B):
+        cs = dict(K=before["K"][:, b], V=before["V"][:, b], H=before["H"][:, b])
+        r = O.reuse_step(shape, W, lat_np[b], 700, 650, tkv_o[b], per[b], cs, lat_next[b], np.array(delta))
+        e = dict(latent=relerr(outs[1][0][b], r["latent_next"]), maps=relerr(outs[1][1][b], r["maps"]))
+        if per[b].size:
+            e.update(H=relerr(got["H"][:, b][:, per[b]], r["H"][:, per[b]]),
+                     K=relerr(got["K"][:, b][:, :, per[b]], r["K"][:, :, per[b]]),
+                     V=relerr(got["V"][:, b][:, :, per[b]], r["V"][:, :, per[b]]))
+            pb = teacher_forced_reuse(shape, W, lat_np[b], 700, tkv_o[b], per[b], cs,
+                                      {k: got[k][:, b] for k in ("K", "V", "H")})
+            assert not gate_failures(pb, 2e-2), b
+            e["per_block_worst_dH"] = summarize(pb)["dH"]
+        _say(f"hosted reuse step vs oracle, chain {b} R={per[b].size}: " + " ".join(f"{k} {v:.2e}" for k, v in e.items()))
+        assert e["latent"] < 2e-2 and e["maps"] < 2e-2 and e.get("H", 0) < 2e-2 and e.get("K", 0) < 2e-2
+        assert e.get("V", 0) < 2e-2
 
     outs = []
     for cache in (dev, host):
@@ -81,3 +104,11 @@ def test_hosted_pool_matches_device_pool():
         outs.append(to_np(out))
     assert np.array_equal(outs[0], outs[1])
     _compare(dev, host, 0, shape.layers, B)
+    got = download_slot(host, 0, shape.layers, B)
+    for b in range(B):
+        r = O.dense_step(shape, W, lat_np[b], 999, 700, tkv_o[b])
+        e = dict(latent=relerr(outs[1][b], r["latent_next"]), H=relerr(got["H"][:, b], r["H"]),
+                 K=relerr(got["K"][:, b], r["K"]), V=relerr(got["V"][:, b], r["V"]))
+        pb = teacher_forced_dense(shape, W, lat_np[b], 999, tkv_o[b], {k: got[k][:, b] for k in ("K", "V", "H")})
+        _say(f"hosted dense step vs oracle, chain {b}: " + " ".join(f"{k} {v:.2e}" for k, v in e.items()))
+        assert max(e.values()) < 2e-2 and not gate_failures(pb, 2e-2), b
