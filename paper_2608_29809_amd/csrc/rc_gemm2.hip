@@ -3,8 +3,12 @@
 //
 // * Operands move global -> LDS with global_load_lds_dwordx4 (no VGPR
 //   staging); every 128-byte K-row of a tile is stored with its eight
-//   16-byte chunks XOR-swizzled by (row & 7), so the MFMA fragment reads
-//   (lane l reads row l%32, chunk 2kk + l/32) hit distinct LDS banks.
+//   16-byte chunks XOR-swizzled by swz(row) = (row >> 1) & 7.  A 16-byte
+//   fragment read (lane l reads row l%32, chunk 2kk + l/32) is served 16
+//   lanes per pass over 64 four-byte banks: rows r..r+15 cover the two
+//   128-byte bank halves by row parity and, within a parity, eight distinct
+//   chunks, so no two lanes of a pass share a bank (an (row & 7) swizzle
+//   gives rows r and r+8 the same banks: two-way conflicts).
 // * STAGES-deep ring of LDS buffers, one barrier per 64-wide K step; loads
 //   for step k+STAGES-1 are issued right after the barrier of step k.
 // * A K group is 4 or 8 waves in a WGM x WGN grid, each wave a
@@ -24,6 +28,9 @@
 namespace rc {
 
 constexpr int G2_BK = 64;  // bf16 elements per K step (128 bytes per row)
+
+// 16-byte chunk swizzle of a tile row in LDS (see the file comment).
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -207,7 +214,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
 #pragma unroll
     for (int i = 0; i < A_LD; ++i) {
       const int ch = (i * NW + w4) * 64 + lane;
-      const int r = ch >> 3, c = (ch & 7) ^ (r & 7);
+      const int r = ch >> 3, c = (ch & 7) ^ swz(r);
       const int gr = min(m0 + r, g.M - 1);
       const bf16 *src = A + (size_t)gr * g.lda + k0 + c * 8;
       __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
@@ -216,7 +223,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
 #pragma unroll
     for (int i = 0; i < B_LD; ++i) {
       const int ch = (i * NW + w4) * 64 + lane;
-      const int r = ch >> 3, c = (ch & 7) ^ (r & 7);
+      const int r = ch >> 3, c = (ch & 7) ^ swz(r);
       const bf16 *src = W + (size_t)(n0 + r) * g.K + k0 + c * 8;
       __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
                                        (__attribute__((address_space(3))) void *)(sb + (i * NW + w4) * 1024), 16, 0, 0);
@@ -250,12 +257,12 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
 #pragma unroll
       for (int i = 0; i < FM; ++i) {
         const int r = wm * WM + i * 32 + r32;
-        a[buf][i] = *(const bf16x8 *)(sa + r * 128 + ((c ^ (r & 7)) << 4));
+        a[buf][i] = *(const bf16x8 *)(sa + r * 128 + ((c ^ swz(r)) << 4));
       }
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
         const int r = wn * WN + j * 32 + r32;
-        b[buf][j] = *(const bf16x8 *)(sb + r * 128 + ((c ^ (r & 7)) << 4));
+        b[buf][j] = *(const bf16x8 *)(sb + r * 128 + ((c ^ swz(r)) << 4));
       }
     };
     frags(0, 0);
@@ -520,6 +527,9 @@ static void launch_reduce(const GemmArgs &a, int epi, int splits, const float *p
 // workgroups per CU.  Split-K over the grid pays only for K = 4608, in two
 // halves up to ~2700 rows (the halves as 128-row tiles while they fit one
 // wave of workgroups); three splits measured slower in the step at 4096 rows.
+// Narrow outputs (N = 1152, K = 1152) at a few hundred to ~900 rows take
+// 64x64 tiles with two K groups of 2x2 waves (216 workgroups at 723 rows:
+// 9.1 against 10.9 us for 32x128 tiles, weights cold).
 GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats) {
   GemmPlan p{64, 128, 1, 1, 2, 2, 2};
   const int nk = K / G2_BK;
@@ -548,7 +558,11 @@ GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats) {
     else set(128, 1, 2, 2, 2);
     return p;
   }
-  if (nk % 2 == 0 && t32 <= 256) set(32, 2, 3, 1, 4);
+  const long t64x64 = (long)((M + 63) / 64) * (N / 64);
+  if (nk % 2 == 0 && M > 256 && N % 64 == 0 && t64x64 <= 256) {
+    set(64, 2, 3, 2, 2);
+    p.bn = 64;
+  } else if (nk % 2 == 0 && t32 <= 256) set(32, 2, 3, 1, 4);
   else if (nk % 2 == 0 && t64 <= 256) set(64, 2, 3, 2, 2);
   else if (t64 <= 512) set(64, 1, 3, 2, 4);
   return p;
@@ -556,28 +570,29 @@ GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats) {
 
 hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &pl, float *partial, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
-  if (pl.bn != 128 || a.N % 128 || a.K % (G2_BK * pl.splits * pl.kg)) return hipErrorInvalidValue;
+  if ((pl.bn != 128 && pl.bn != 64) || a.N % pl.bn || a.K % (G2_BK * pl.splits * pl.kg)) return hipErrorInvalidValue;
   const bool split = pl.splits > 1;
   // 4-wave K groups: 128 rows = 2x2 waves of 64x64, 64 rows = 2x2 of 32x64,
-  // 32 rows = 1x4 of 32x32; 8-wave: 128 rows = 4x2 of 32x64 or 2x4 of 64x32,
-  // 64 rows = 2x4 of 32x32
-#define RC_G2(BMV, KGV, STG, WM_, WN_)                                                       \
+  // 32 rows = 1x4 of 32x32, 64x64 tiles = 2x2 of 32x32; 8-wave: 128 rows =
+  // 4x2 of 32x64 or 2x4 of 64x32, 64 rows = 2x4 of 32x32
+#define RC_G2(BMV, BNV, KGV, STG, WM_, WN_)                                                   \
   {                                                                                          \
-    if (split) launch_g2<BMV, 128, STG, KGV, WM_, WN_, true>(a, epi, pl.splits, partial, s); \
-    else launch_g2<BMV, 128, STG, KGV, WM_, WN_, false>(a, epi, 1, nullptr, s);              \
+    if (split) launch_g2<BMV, BNV, STG, KGV, WM_, WN_, true>(a, epi, pl.splits, partial, s); \
+    else launch_g2<BMV, BNV, STG, KGV, WM_, WN_, false>(a, epi, 1, nullptr, s);              \
   }
-  const int cfg = pl.bm * 10000 + pl.kg * 1000 + pl.stages * 100 + pl.wgm * 10 + pl.wgn;
+  const long cfg = pl.bn * 10000000L + pl.bm * 10000 + pl.kg * 1000 + pl.stages * 100 + pl.wgm * 10 + pl.wgn;
   switch (cfg) {
-    case 641222: RC_G2(64, 1, 2, 2, 2) break;
-    case 642322: RC_G2(64, 2, 3, 2, 2) break;
-    case 641324: RC_G2(64, 1, 3, 2, 4) break;
-    case 321314: RC_G2(32, 1, 3, 1, 4) break;
-    case 322314: RC_G2(32, 2, 3, 1, 4) break;
-    case 323214: RC_G2(32, 3, 2, 1, 4) break;
-    case 1281222: RC_G2(128, 1, 2, 2, 2) break;
-    case 1281242: RC_G2(128, 1, 2, 4, 2) break;
-    case 1281342: RC_G2(128, 1, 3, 4, 2) break;
-    case 1281324: RC_G2(128, 1, 3, 2, 4) break;
+    case 1280641222: RC_G2(64, 128, 1, 2, 2, 2) break;
+    case 1280642322: RC_G2(64, 128, 2, 3, 2, 2) break;
+    case 1280641324: RC_G2(64, 128, 1, 3, 2, 4) break;
+    case 1280321314: RC_G2(32, 128, 1, 3, 1, 4) break;
+    case 1280322314: RC_G2(32, 128, 2, 3, 1, 4) break;
+    case 1280323214: RC_G2(32, 128, 3, 2, 1, 4) break;
+    case 1281281222: RC_G2(128, 128, 1, 2, 2, 2) break;
+    case 1281281242: RC_G2(128, 128, 1, 2, 4, 2) break;
+    case 1281281342: RC_G2(128, 128, 1, 3, 4, 2) break;
+    case 1281281324: RC_G2(128, 128, 1, 3, 2, 4) break;
+    case 640642322: RC_G2(64, 64, 2, 3, 2, 2) break;
     default: return hipErrorInvalidValue;
   }
 #undef RC_G2
