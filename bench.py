@@ -193,22 +193,25 @@ def main():
                                                       for k, v in sorted(per.items(), key=lambda kv: -kv[1]['total_ms'])))
 
     C, N, F, M = shape.hidden, shape.tokens, shape.mlp, shape.text_len
-    flops_per_launch = {  # algorithmic flops of one launch at R active rows (one chain)
-        "attn_self": 4.0 * R * N * C,
-        "attn_cross": 4.0 * R * M * C,
-        "gemm_qkv": 2.0 * R * 3 * C * C,
-        "gemm_fc1": 2.0 * R * F * C,
-        "gemm_fc2": 2.0 * R * C * F,
-        "gemm_proj": 2.0 * R * C * C,
-        "gemm_xq": 2.0 * R * C * C,
-        "gemm_xproj": 2.0 * R * C * C,
-    }
-    dom = max((k for k in per if k in flops_per_launch), key=lambda k: per[k]["total_ms"])
-    achieved = flops_per_launch[dom] / (per[dom]["avg_us"] * 1e-6) / 1e12
+    work = class_work(shape, R, 1)
+    by_class = {}
+    for k, w in work.items():
+        if k not in per:
+            continue
+        sec = per[k]["avg_us"] * 1e-6
+        e = dict(bound=w["bound"], avg_launch_us=round(per[k]["avg_us"], 3), launches_per_step=per[k]["launches"],
+                 flops_per_launch=w["flops"], bytes_per_launch=w["bytes"],
+                 tflops=round(w["flops"] / sec / 1e12, 2), gbs=round(w["bytes"] / sec / 1e9, 1))
+        e["frac"] = round(e["tflops"] / PEAK_BF16_TFLOPS if w["bound"] == "mfma" else e["gbs"] / PEAK_HBM_GBS, 4)
+        by_class[k] = e
+    mfma_classes = [k for k in by_class if by_class[k]["bound"] == "mfma"]
+    dom = max(mfma_classes, key=lambda k: per[k]["total_ms"])
+    achieved = by_class[dom]["tflops"]
     traffic = _committed_traffic(dom, R)
-    roofline = dict(bound="mfma", kernel=dom, achieved=round(achieved, 2), peak=PEAK_BF16_TFLOPS,
+    roofline = dict(bound="mfma", kernel=dom, achieved=achieved, peak=PEAK_BF16_TFLOPS,
                     unit="TFLOP/s", frac=round(achieved / PEAK_BF16_TFLOPS, 4), traffic=traffic,
-                    flops_per_launch=flops_per_launch[dom], avg_launch_us=round(per[dom]["avg_us"], 3))
+                    flops_per_launch=work[dom]["flops"], avg_launch_us=by_class[dom]["avg_launch_us"])
+    log("roofline by class: " + ", ".join(f"{k} {v['frac']:.3f}" for k, v in sorted(by_class.items(), key=lambda kv: -per[kv[0]]["total_ms"])))
 
     # ---------------------------------------------------------------- whole editing turn
     schedule = None
@@ -288,6 +291,7 @@ def main():
         "schedule": schedule,
         "kernels_ms_per_step": {k: round(v["total_ms"], 4) for k, v in per.items()},
         "roofline": roofline,
+        "roofline_by_class": by_class,
         "localize": loc,
         "fraction_sweep": sweep,
         "resolution_sweep": res,
@@ -428,8 +432,14 @@ def resolution_leg(W, args):
 
         dense_ms = timed(lambda: model.build_cache(cache, 0, lat, 842, 789, tkv, latent_out=nxt))
         reuse_ms = timed(lambda: model.reuse_step(cache, 0, act, lat, 842, 789, tkv, latent_out=nxt))
+        # bytes a reuse step must move: every block's weights once, the slot's
+        # keys and values, the fresh keys, values and hidden rows written back
+        C_, L_, R_ = shape.hidden, shape.layers, int(act.total)
+        nbytes = L_ * 14 * C_ * C_ * 2 + 2 * L_ * g * g * C_ * 2 + 3 * L_ * R_ * C_ * 2
+        gbs = nbytes / (reuse_ms * 1e-3) / 1e9
         out[f"{px}px"] = dict(tokens=g * g, active=int(act.total), reuse_step_ms=round(reuse_ms, 3),
-                              dense_step_ms=round(dense_ms, 3), speedup=round(dense_ms / reuse_ms, 3))
+                              dense_step_ms=round(dense_ms, 3), speedup=round(dense_ms / reuse_ms, 3),
+                              reuse_bytes=nbytes, reuse_gbs=round(gbs, 1), hbm_frac=round(gbs / PEAK_HBM_GBS, 4))
         log(f"{px} px: {g * g} tokens, {act.total} active: reuse {reuse_ms:.3f} ms, dense {dense_ms:.3f} ms")
         del cache, model
         torch.cuda.empty_cache()
@@ -467,7 +477,7 @@ def sweep_leg(model1, args):
         torch.cuda.synchronize()
         return ev[0].elapsed_time(ev[1]) / n
 
-    out = {}
+    out, rows = {}, {}
     steps = list(range(4, T))
     for f in (0.05, 0.10, 0.25, 0.50, 1.00):
         act = ActiveSet.from_lists(synth.sweep_regions(args.seed, f, B))
@@ -478,6 +488,7 @@ def sweep_leg(model1, args):
                              latent_out=lat[s + 1])
 
         out[f"{int(f * 100)}%"] = round(timed(rs, 8), 3)
+        rows[f"{int(f * 100)}%"] = act.total
     def ds(k):
         s = steps[k % len(steps)]
         model.build_cache(cache, s, lat[s], int(tgrid[s]), int(tgrid[s + 1]) if s + 1 < T else -1, tkv,
@@ -485,10 +496,88 @@ def sweep_leg(model1, args):
     dense_ms = round(timed(ds, 4), 3)
     log("fraction sweep (batch 4, ms per step): " + ", ".join(f"{k} {v}" for k, v in out.items()) +
         f"; dense {dense_ms}")
+    # fixed per-step cost: least-squares line t = a + b * rows over the
+    # partial fractions (5-50 %); a is the step time at zero active rows
+    keys = [k for k in out if k != "100%"]
+    xs = np.array([rows[k] for k in keys], float)
+    ys = np.array([out[k] for k in keys], float)
+    b_ms, a_ms = np.polyfit(xs, ys, 1)
+    log(f"fraction sweep intercept: {a_ms:.3f} ms + {b_ms * 1000:.3f} us per active row")
+
+    # the configured workload: per fraction, four edit turns (turn 0 is the
+    # dense trajectory above), each with fresh blob masks and fresh delta
+    # tokens, a 20-step schedule of 4 dense steps then 16 region-reuse steps;
+    # against all-dense turns
+    sched = {}
+    n_dense = 4
+    txt_prev = txt
+
+    def one_turn(txt_t, act_t, all_dense):
+        tk = model.prepare_text(model.to_storage(txt_t))
+        for s in range(T):
+            tn = int(tgrid[s + 1]) if s + 1 < T else -1
+            if all_dense or s < n_dense:
+                model.build_cache(cache, s, lat[s], int(tgrid[s]), tn, tk, latent_out=lat[s + 1])
+            else:
+                model.reuse_step(cache, s, act_t, lat[s], int(tgrid[s]), tn, tk, latent_out=lat[s + 1])
+
+    for f in (0.05, 0.10, 0.25, 0.50, 1.00):
+        per_turn = []
+        for turn in range(1, 5):
+            txt_t, _ = synth.edit_text(shape, txt_prev, 5, args.seed + 100 * turn + int(f * 100))
+            act_t = ActiveSet.from_lists(synth.sweep_regions(args.seed + turn, f, B))
+            torch.cuda.synchronize()
+            ev[0].record()
+            one_turn(txt_t, act_t, False)
+            ev[1].record()
+            torch.cuda.synchronize()
+            per_turn.append(ev[0].elapsed_time(ev[1]))
+            txt_prev = txt_t
+        sched[f"{int(f * 100)}%"] = round(float(np.mean(per_turn)), 2)
+    ev[0].record()
+    one_turn(txt_prev, None, True)
+    ev[1].record()
+    torch.cuda.synchronize()
+    dense_turn_ms = ev[0].elapsed_time(ev[1])
+    log("edit turns (batch 4, 4 dense + 16 reuse, ms per turn): " + ", ".join(f"{k} {v}" for k, v in sched.items()) +
+        f"; all-dense turn {dense_turn_ms:.1f}")
     del cache
     torch.cuda.empty_cache()
-    return dict(batch=B, reuse_step_ms=out, dense_step_ms=dense_ms,
-                speedup_vs_dense={k: round(dense_ms / v, 3) for k, v in out.items()})
+    return dict(batch=B, active_rows=rows, reuse_step_ms=out, dense_step_ms=dense_ms,
+                speedup_vs_dense={k: round(dense_ms / v, 3) for k, v in out.items()},
+                fixed_ms=round(float(a_ms), 3), per_active_row_us=round(float(b_ms) * 1000, 4),
+                edit_turns=dict(turns_per_fraction=4, steps=T, dense_steps=n_dense, masks="fresh blob masks per turn",
+                                turn_ms=sched, all_dense_turn_ms=round(dense_turn_ms, 2),
+                                speedup_vs_all_dense={k: round(dense_turn_ms / v, 3) for k, v in sched.items()}))
+
+
+def class_work(shape, R, B):
+    """Algorithmic work of one launch of each kernel class of a region step
+    over R active rows in B chains (one chain's worth of keys per chain):
+    flops for the matrix-core classes, bytes every launch must move at least
+    once for the memory-bound ones (and for the GEMMs, whose weights are
+    streamed from HBM once per launch).  bf16 operands, fp32 residual stream."""
+    C, N, F, M, H = shape.hidden, shape.tokens, shape.mlp, shape.text_len, shape.heads
+    e = 2  # bf16
+
+    def g(m, n, k, out_bytes, extra_in=0):
+        return dict(bound="mfma", flops=2.0 * m * n * k, bytes=n * k * e + m * k * e + out_bytes + extra_in)
+    w = {
+        "gemm_qkv": g(R, 3 * C, C, R * 3 * C * e),                      # q compact, k/v scattered into the slot
+        "gemm_proj": g(R, C, C, R * C * (4 + e), R * C * 4),            # X read + written, bf16 copy
+        "gemm_xq": g(R, C, C, R * C * e),
+        "gemm_xproj": g(R, C, C, R * C * 4, R * C * 4),                 # X read + written
+        "gemm_fc1": g(R, F, C, R * F * e),
+        "gemm_fc2": g(R, C, F, 2 * R * C * 4),                          # two fp32 split partials
+        "attn_self": dict(bound="mfma", flops=4.0 * R * N * C,
+                          bytes=B * 2 * H * N * 72 * e + R * C * e + 5 * R * C * e),  # K,V of the slot, Q, split outputs
+        "attn_cross": dict(bound="mfma", flops=4.0 * R * M * C, bytes=B * 2 * C * 128 * e + 2 * R * C * e),
+        "attn_combine": dict(bound="hbm", flops=0.0, bytes=5 * R * C * e + R * C * e),
+        "split_finish": dict(bound="hbm", flops=0.0, bytes=2 * R * C * 4 + 2 * R * C * 4 + 2 * R * C * e),
+        "norm": dict(bound="hbm", flops=0.0, bytes=R * C * (4 + e)),
+        "embed": dict(bound="hbm", flops=0.0, bytes=R * C * 4 + R * 16 * 4),
+    }
+    return w
 
 
 KERNEL_SOURCES = {  # sources whose text fixes a kernel class's code
@@ -526,18 +615,30 @@ def _committed_traffic(cls, R):
     return None
 
 
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(shape, W, idx, args):
-    """The float64 oracle timed on this machine's host cores on a bounded
-    sample of the same reuse step: the first `--cpu-layers` blocks of the step
-    for one chain; the per-step time is scaled by layers/sampled-layers."""
+    """The oracle, in its float32 mode, timed on this machine's host cores on
+    a bounded sample of the same reuse step: the first `--cpu-layers` blocks
+    of the step for one chain; the per-step time is scaled by
+    layers/sampled-layers."""
     import dataclasses
     import oracle as O
     import synth
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        blas = sorted({i.get("internal_api", "?") for i in threadpool_info()})
     except Exception:
-        threads = os.cpu_count()
+        threads, blas = os.cpu_count(), []
     Ls = max(1, min(args.cpu_layers, shape.layers))
     sub = dataclasses.replace(shape, layers=Ls)
     Wsub = dict(W)
@@ -546,19 +647,21 @@ def cpu_baseline(shape, W, idx, args):
     lat = synth.make_latent(shape, 1, args.seed)
     slot = synth.make_cache_slot(sub, 1, args.seed)
     cache = dict(K=slot["K"][:, 0], V=slot["V"][:, 0], H=slot["H"][:, 0])
-    y = O.caption_projection(Wsub, txt[0])
-    tkv = [O.text_kv(lw, y, shape.heads) for lw in Wsub["layers"]]
+    f32 = np.float32
+    y = O.caption_projection(Wsub, txt[0], dt=f32)
+    tkv = [O.text_kv(lw, y, shape.heads, dt=f32) for lw in Wsub["layers"]]
     w0 = time.perf_counter()
-    O.reuse_step(sub, Wsub, lat[0], 842, 789, tkv, idx, cache, lat[0])
+    O.reuse_step(sub, Wsub, lat[0], 842, 789, tkv, idx, cache, lat[0], dt=f32)
     dt = time.perf_counter() - w0
     per_step = dt * shape.layers / Ls
-    log(f"oracle: {Ls} blocks in {dt:.2f}s -> {per_step:.2f}s per {shape.layers}-block reuse step")
+    log(f"oracle (float32): {Ls} blocks in {dt:.2f}s -> {per_step:.2f}s per {shape.layers}-block reuse step")
     blocks = (f"all {Ls} blocks" if Ls == shape.layers
               else f"first {Ls} of {shape.layers} blocks, time x {shape.layers}/{Ls}")
     return dict(value=round(1.0 / per_step, 5), unit="steps/s", cores=int(threads), kind="oracle",
                 sample=f"one region-reuse step of one chain, {blocks} (R={len(idx)} of {shape.tokens} tokens), "
-                       f"float64 NumPy",
-                sample_seconds=round(dt, 3))
+                       f"float32 NumPy",
+                sample_seconds=round(dt, 3), nproc=len(os.sched_getaffinity(0)), cpu_model=_cpu_model(),
+                blas=blas)
 
 
 if __name__ == "__main__":

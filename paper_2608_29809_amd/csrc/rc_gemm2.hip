@@ -529,7 +529,9 @@ static void launch_reduce(const GemmArgs &a, int epi, int splits, const float *p
 // wave of workgroups); three splits measured slower in the step at 4096 rows.
 // Narrow outputs (N = 1152, K = 1152) at a few hundred to ~900 rows take
 // 64x64 tiles with two K groups of 2x2 waves (216 workgroups at 723 rows:
-// 9.1 against 10.9 us for 32x128 tiles, weights cold).
+// 9.1 against 10.9 us for 32x128 tiles, weights cold).  A four-deep ring
+// gains ~3 % over three for these and for the 4x2-wave 128x128 QKV tiles
+// (16.3 against 16.8 us), and nothing for the 2x4-wave MLP-up tiles.
 GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats) {
   GemmPlan p{64, 128, 1, 1, 2, 2, 2};
   const int nk = K / G2_BK;
@@ -553,14 +555,15 @@ GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats) {
   }
   if (N >= 3072) {
     if (t64 <= 256) set(64, 1, 3, 2, 4);
-    else if (t128 <= 256) set(128, 1, 3, N % 512 ? 4 : 2, N % 512 ? 2 : 4);
+    else if (t128 <= 256 && N % 512) set(128, 1, 4, 4, 2);
+    else if (t128 <= 256) set(128, 1, 3, 2, 4);
     else if (M < 3072) set(128, 1, 2, 4, 2);
     else set(128, 1, 2, 2, 2);
     return p;
   }
   const long t64x64 = (long)((M + 63) / 64) * (N / 64);
   if (nk % 2 == 0 && M > 256 && N % 64 == 0 && t64x64 <= 256) {
-    set(64, 2, 3, 2, 2);
+    set(64, 2, 4, 2, 2);
     p.bn = 64;
   } else if (nk % 2 == 0 && t32 <= 256) set(32, 2, 3, 1, 4);
   else if (nk % 2 == 0 && t64 <= 256) set(64, 2, 3, 2, 2);
@@ -592,7 +595,8 @@ hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &pl, float *p
     case 1281281242: RC_G2(128, 128, 1, 2, 4, 2) break;
     case 1281281342: RC_G2(128, 128, 1, 3, 4, 2) break;
     case 1281281324: RC_G2(128, 128, 1, 3, 2, 4) break;
-    case 640642322: RC_G2(64, 64, 2, 3, 2, 2) break;
+    case 640642422: RC_G2(64, 64, 2, 4, 2, 2) break;
+    case 1281281442: RC_G2(128, 128, 1, 4, 4, 2) break;
     default: return hipErrorInvalidValue;
   }
 #undef RC_G2
