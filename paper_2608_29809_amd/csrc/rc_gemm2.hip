@@ -529,24 +529,34 @@ static void launch_reduce(const GemmArgs &a, int epi, int splits, const float *p
 // wave of workgroups); three splits measured slower in the step at 4096 rows.
 // Narrow outputs (N = 1152, K = 1152) at a few hundred to ~900 rows take
 // 64x64 tiles with two K groups of 2x2 waves (216 workgroups at 723 rows:
-// 9.1 against 10.9 us for 32x128 tiles, weights cold).  A four-deep ring
-// gains ~3 % over three for these and for the 4x2-wave 128x128 QKV tiles
-// (16.3 against 16.8 us), and nothing for the 2x4-wave MLP-up tiles.
+// 9.1 against 10.9 us for 32x128 tiles, weights cold), and below ~450 rows
+// 32x64 tiles with two K groups of two waves (8.3 against 10.6 us at 154
+// rows).  The wide outputs below ~250 rows take the 64x64 two-group tiles
+// too (QKV at 154 rows: 9.6 against 13.2 us), and the MLP-down at a few
+// hundred rows four K quarters (12.4 against 18.8 us at 154 rows).  A
+// four-deep ring gains ~3 % over three for the 64x64 tiles and for the
+// 4x2-wave 128x128 QKV tiles (16.3 against 16.8 us), nothing for the
+// 2x4-wave MLP-up tiles.  Two K groups of 2x2 waves beat one group of 2x4
+// for 64x128 tiles at ~400 rows (13.3 against 13.6 us).
 GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats) {
   GemmPlan p{64, 128, 1, 1, 2, 2, 2};
   const int nk = K / G2_BK;
   const long tn = N / 128;
   const long t32 = (long)((M + 31) / 32) * tn, t64 = (long)((M + 63) / 64) * tn, t128 = (long)((M + 127) / 128) * tn;
+  const long t64x64 = (long)((M + 63) / 64) * (N / 64), t32x64 = (long)((M + 31) / 32) * (N / 64);
   auto set = [&](int bm, int kg, int stages, int wgm, int wgn) {
     p.bm = bm; p.kg = kg; p.stages = stages; p.wgm = wgm; p.wgn = wgn;
   };
   if (K >= 2048) {
-    const bool room = (size_t)2 * M * N <= partial_cap_floats;
-    if (t64 < 160 && nk % 4 == 0 && room) {
+    const bool room2 = (size_t)2 * M * N <= partial_cap_floats, room4 = (size_t)4 * M * N <= partial_cap_floats;
+    if (t32 * 4 <= 256 && nk % 8 == 0 && room4) {
+      p.splits = 4;  // a few hundred rows: four K quarters keep ~180 workgroups busy
+      set(32, 2, 3, 1, 4);
+    } else if (t64 < 160 && nk % 4 == 0 && room2) {
       p.splits = 2;
       if (t32 * 2 <= 256) set(32, 2, 3, 1, 4);
       else set(64, 2, 3, 2, 2);
-    } else if (t64 < 384 && nk % 2 == 0 && room) {
+    } else if (t64 < 384 && nk % 2 == 0 && room2) {
       p.splits = 2;
       if (t128 * 2 <= 256) set(128, 1, 3, 2, 4);
       else set(64, 1, 2, 2, 2);
@@ -554,15 +564,21 @@ GemmPlan plan_gemm2(int M, int N, int K, size_t partial_cap_floats) {
     return p;
   }
   if (N >= 3072) {
-    if (t64 <= 256) set(64, 1, 3, 2, 4);
+    if (nk % 2 == 0 && N % 64 == 0 && t64x64 <= 256) {  // ~250 rows and fewer
+      set(64, 2, 4, 2, 2);
+      p.bn = 64;
+    } else if (nk % 2 == 0 && t64 <= 256) set(64, 2, 3, 2, 2);
+    else if (t64 <= 256) set(64, 1, 3, 2, 4);
     else if (t128 <= 256 && N % 512) set(128, 1, 4, 4, 2);
     else if (t128 <= 256) set(128, 1, 3, 2, 4);
     else if (M < 3072) set(128, 1, 2, 4, 2);
     else set(128, 1, 2, 2, 2);
     return p;
   }
-  const long t64x64 = (long)((M + 63) / 64) * (N / 64);
-  if (nk % 2 == 0 && M > 256 && N % 64 == 0 && t64x64 <= 256) {
+  if (nk % 2 == 0 && N % 64 == 0 && t32x64 <= 256) {  // up to ~450 rows at N = 1152
+    set(32, 2, 3, 1, 2);
+    p.bn = 64;
+  } else if (nk % 2 == 0 && M > 256 && N % 64 == 0 && t64x64 <= 256) {
     set(64, 2, 4, 2, 2);
     p.bn = 64;
   } else if (nk % 2 == 0 && t32 <= 256) set(32, 2, 3, 1, 4);
@@ -596,6 +612,7 @@ hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &pl, float *p
     case 1281281342: RC_G2(128, 128, 1, 3, 4, 2) break;
     case 1281281324: RC_G2(128, 128, 1, 3, 2, 4) break;
     case 640642422: RC_G2(64, 64, 2, 4, 2, 2) break;
+    case 640322312: RC_G2(32, 64, 2, 3, 1, 2) break;
     case 1281281442: RC_G2(128, 128, 1, 4, 4, 2) break;
     default: return hipErrorInvalidValue;
   }
