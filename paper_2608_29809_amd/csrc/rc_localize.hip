@@ -10,79 +10,95 @@
 
 namespace rc {
 
-constexpr int LG_TOK = 64;  // tokens per workgroup, 16 per wave
+constexpr int LG_TOK = 16;  // tokens per workgroup, 4 per wave
+constexpr int LG_HC = 4;    // heads whose rows a wave loads at once
+
+// Max and sum over the 16 lanes of a DPP row, in the vector ALU (no LDS
+// permute): neighbours, pairs, half-row mirror, row mirror.  Every step
+// combines two partial results that both lanes of a pair hold bit for bit,
+// so all 16 lanes end with the same value.
+template <int CTRL> __device__ __forceinline__ float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+// IEEE maximum (NaN-propagating): one v_maximum3/v_maximum on gfx950, with
+// no operand canonicalisation as fmaxf needs.
+__device__ __forceinline__ float fmax_(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmax_(v, dpp_mov<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = fmax_(v, dpp_mov<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = fmax_(v, dpp_mov<0x141>(v));  // row_half_mirror
+  return fmax_(v, dpp_mov<0x140>(v));  // row_mirror
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_mov<0xB1>(v);
+  v += dpp_mov<0x4E>(v);
+  v += dpp_mov<0x141>(v);
+  return v + dpp_mov<0x140>(v);
+}
 
 // partial[l][tok][j] = sum_h softmax(Z[l][h][tok][:])[delta_j].  One
-// workgroup per (64-token tile, layer), each wave 16 tokens.  A row of the
+// workgroup per (16-token tile, layer), each wave 4 tokens.  A row of the
 // logits (text_len <= 128 bf16, 16-byte chunks) is spread over one 16-lane
-// group, so a load instruction covers four consecutive rows -- contiguous
-// memory -- and the row's max and sum are 16-lane reductions.  Lane j of a
-// group owns delta column j: it re-reads that one logit (a cache hit) and
-// accumulates its probability.  The next head's rows are loaded while the
-// current head is reduced.
+// group (one token per group), so one load instruction covers four
+// consecutive rows -- contiguous memory -- and the row's max and sum are
+// 16-lane DPP reductions.  A wave issues the rows of LG_HC heads before it
+// reduces any (4 KB in flight per wave at 40 VGPRs, eight waves per SIMD).
+// The exponent runs on the raw v_exp_f32: its argument z - max is <= 0, so a
+// flushed denormal moves a row sum that is >= 1 by less than 2^-126, and the
+// row's reciprocal is one v_rcp_f32 (1 ulp).  Lane j of a group owns delta
+// column j: it re-reads that one logit (a cache hit) and accumulates its
+// probability over the heads in order.
 __global__ __launch_bounds__(256) void maps_from_logits_kernel(const uint16_t *Z, int heads, int tokens,
                                                                int text_len, MapsDelta dl, float *partial) {
   const int l = blockIdx.y, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int grp = lane >> 4, j16 = lane & 15;
-  const int tok_w = blockIdx.x * LG_TOK + wave * 16;  // first token of this wave
-  const int row_vec = text_len / 8;                    // 16-byte chunks per row
-  const bool lane_on = j16 < row_vec;
-  const bool owner = j16 < dl.n;
+  const int tok = blockIdx.x * LG_TOK + wave * 4 + grp;  // this lane group's token
+  const int row_vec = text_len / 8;                       // 16-byte chunks per row
+  const bool ok = tok < tokens;
+  const bool lane_on = j16 < row_vec && ok;
+  const bool owner = j16 < dl.n && ok;
   int my_col = 0;
 #pragma unroll
   for (int j = 0; j < 8; ++j)
     if (j == j16) my_col = dl.col[j];
   constexpr float kLog2e = 1.4426950408889634f;
-  auto load = [&](int h, V16 *v, uint16_t *zd) {
-    const uint16_t *blk = Z + ((size_t)(l * heads + h) * tokens + tok_w) * text_len;
+  float acc = 0.0f;
+  for (int h0 = 0; h0 < heads; h0 += LG_HC) {
+    V16 v[LG_HC];
+    uint16_t zd[LG_HC];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = i * 4 + grp;
-      const bool ok = tok_w + row < tokens;
-      v[i] = V16{{0u, 0u, 0u, 0u}};
-      if (lane_on && ok) v[i] = *(const V16 *)(blk + (size_t)row * text_len + j16 * 8);
-      zd[i] = (owner && ok) ? blk[(size_t)row * text_len + my_col] : (uint16_t)0;
+    for (int c = 0; c < LG_HC; ++c) {
+      const uint16_t *row = Z + ((size_t)(l * heads + h0 + c) * tokens + tok) * text_len;
+      const bool on = h0 + c < heads;
+      v[c] = V16{{0u, 0u, 0u, 0u}};
+      if (on && lane_on) v[c] = *(const V16 *)(row + j16 * 8);
+      zd[c] = (on && owner) ? row[my_col] : (uint16_t)0;
     }
-  };
-  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  V16 cur[4], nxt[4];
-  uint16_t zc[4], zn[4];
-  load(0, cur, zc);
-  for (int h = 0; h < heads; ++h) {
-    if (h + 1 < heads) load(h + 1, nxt, zn);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int c = 0; c < LG_HC; ++c) {
+      const bool on = h0 + c < heads;
       float z[8];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        z[2 * q] = __uint_as_float(cur[i].w[q] << 16);
-        z[2 * q + 1] = __uint_as_float(cur[i].w[q] & 0xFFFF0000u);
+        z[2 * q] = __uint_as_float(v[c].w[q] << 16);
+        z[2 * q + 1] = __uint_as_float(v[c].w[q] & 0xFFFF0000u);
       }
       float m = -INFINITY;
-      if (lane_on)
-        m = fmaxf(fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3])), fmaxf(fmaxf(z[4], z[5]), fmaxf(z[6], z[7])));
-#pragma unroll
-      for (int o = 8; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 16));
+      if (on && lane_on)
+        m = fmax_(fmax_(fmax_(z[0], z[1]), fmax_(z[2], z[3])), fmax_(fmax_(z[4], z[5]), fmax_(z[6], z[7])));
+      m = row16_max(m);
       const float mc = m * kLog2e;
       float sum = 0.0f;
-      if (lane_on)
+      if (on && lane_on)
 #pragma unroll
-        for (int q = 0; q < 8; ++q) sum += exp2f(__builtin_fmaf(z[q], kLog2e, -mc));
-#pragma unroll
-      for (int o = 8; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 16);
-      if (owner) acc[i] += exp2f(__builtin_fmaf(__uint_as_float((uint32_t)zc[i] << 16), kLog2e, -mc)) / sum;
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      cur[i] = nxt[i];
-      zc[i] = zn[i];
+        for (int q = 0; q < 8; ++q) sum += __builtin_amdgcn_exp2f(__builtin_fmaf(z[q], kLog2e, -mc));
+      sum = row16_sum(sum);
+      if (on && owner)
+        acc += __builtin_amdgcn_exp2f(__builtin_fmaf(__uint_as_float((uint32_t)zd[c] << 16), kLog2e, -mc)) *
+               __builtin_amdgcn_rcpf(sum);
     }
   }
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int tok = tok_w + i * 4 + grp;
-    if (owner && tok < tokens) partial[((size_t)l * tokens + tok) * dl.n + j16] = acc[i];
-  }
+  if (owner) partial[((size_t)l * tokens + tok) * dl.n + j16] = acc;
 }
 
 hipError_t launch_maps_from_logits(const uint16_t *logits, int n_layers, int heads, int tokens, int text_len,
