@@ -571,7 +571,9 @@ def class_work(shape, R, B):
         "gemm_fc2": g(R, C, F, 2 * R * C * 4),                          # two fp32 split partials
         "attn_self": dict(bound="mfma", flops=4.0 * R * N * C,
                           bytes=B * 2 * H * N * 72 * e + R * C * e + 5 * R * C * e),  # K,V of the slot, Q, split outputs
-        "attn_cross": dict(bound="mfma", flops=4.0 * R * M * C, bytes=B * 2 * C * 128 * e + 2 * R * C * e),
+        # the cross query projection runs inside the bf16 cross-attention kernel
+        "attn_cross": dict(bound="mfma", flops=4.0 * R * M * C + 2.0 * R * C * C,
+                           bytes=B * 2 * C * 128 * e + C * C * e + 2 * R * C * e),  # text K/V, Wq, rows in, out
         "attn_combine": dict(bound="hbm", flops=0.0, bytes=5 * R * C * e + R * C * e),
         "split_finish": dict(bound="hbm", flops=0.0, bytes=2 * R * C * 4 + 2 * R * C * 4 + 2 * R * C * e),
         "norm": dict(bound="hbm", flops=0.0, bytes=R * C * (4 + e)),

@@ -373,7 +373,8 @@ enum {
   RC_KC_GEMM = 0, RC_KC_ATTN_SELF = 1, RC_KC_ATTN_CROSS = 2, RC_KC_ATTN_COMBINE = 3,
   RC_KC_NORM = 4, RC_KC_EMBED = 5, RC_KC_FINAL = 6, RC_KC_COND = 7, RC_KC_MISC = 8,
   RC_KC_GEMM_QKV = 9, RC_KC_GEMM_FC1 = 10, RC_KC_GEMM_FC2 = 11, RC_KC_GEMM_PROJ = 12,
-  RC_KC_GEMM_XQ = 13, RC_KC_GEMM_XPROJ = 14,
+  RC_KC_GEMM_XQ = 13, /* float32 contexts only: bf16 projects the cross query inside RC_KC_ATTN_CROSS */
+  RC_KC_GEMM_XPROJ = 14,
   RC_KC_SPLIT_FINISH = 15, /* sum of a split-K GEMM's partials (+ the next block's LayerNorm) */
   RC_KC_COUNT = 16
 };

@@ -516,11 +516,9 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       g.warm = lw.xproj_w; g.warm_lines = wlines(C, C);
       RC_TRY(gemm<T>(c, RC_KC_GEMM_PROJ, g, rc::EPI_RESID, gpart, gpf, s));
     }
-    {  // cross-attention query
+    if (sizeof(T) != 2) {  // cross-attention query (bf16: projected inside the cross-attention)
       rc::GemmArgs g{};
       g.A = A1; g.W = lw.xq_w; g.bias = lw.xq_b; g.M = R; g.N = C; g.K = C; g.lda = C; g.out = Q; g.ldo = C;
-      if (dense) { g.warm = lw.fc1_w; g.warm_lines = wlines(F, C); }
-      else { g.warm = lw.fc2_w; g.warm_lines = fc2_half; }
       RC_TRY(gemm<T>(c, RC_KC_GEMM_XQ, g, rc::EPI_STORE, gpart, gpf, s));
     }
     {  // cross-attention to the text, emitting the delta-token maps
@@ -531,14 +529,16 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       a.offsets = offsets_dev; a.n_keys = c->Mp; a.n_valid = c->M; a.text_valid = io->text_valid;
       a.hidden = C; a.splits = 1;
       a.O = O; a.total_rows = R; a.scale_log2 = scale_log2;
-      if (dense) { a.warm = lw.fc2_w; a.warm_lines = fc2_lines; }
+      a.q_x = A1; a.q_w = lw.xq_w; a.q_b = lw.xq_b;
+      if (dense) { a.warm = lw.fc1_w; a.warm_lines = wlines(F, C); }
+      else { a.warm = lw.fc2_w; a.warm_lines = fc2_half; }
       if (emit) {
         a.n_delta = io->n_delta;
         for (int j = 0; j < io->n_delta; ++j) a.delta[j] = io->delta_cols_host[j];
         a.pmaps = pmaps;
       }
       RC_TRY(timed(c, RC_KC_ATTN_CROSS, s, [&] {
-        return sizeof(T) == 2 ? rc::launch_attention2(a, B, max_rb, s)
+        return sizeof(T) == 2 ? rc::launch_attention2q(a, B, max_rb, s)
                               : rc::launch_attention<T>(a, B, max_rb, emit, s);
       }));
       if (emit)
@@ -551,6 +551,7 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       g.A = O; g.W = lw.xproj_w; g.bias = lw.xproj_b; g.M = R; g.N = C; g.K = C; g.lda = C;
       g.X = X; g.ldx = C;
       if (!dense) { g.warm = (const char *)lw.fc2_w + fc2_half * 128; g.warm_lines = fc2_lines - fc2_half; }
+      else { g.warm = lw.fc2_w; g.warm_lines = fc2_lines; }
       RC_TRY(gemm<T>(c, RC_KC_GEMM_XPROJ, g, rc::EPI_RESID, gpart, gpf, s));
     }
     RC_TRY(timed(c, RC_KC_NORM, s, [&] { return rc::launch_ln_mod<T>(X, R, C, lw.sst, t0, 3, c->cfg.ln_eps, A1, s); }));

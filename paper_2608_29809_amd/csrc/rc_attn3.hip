@@ -2,12 +2,14 @@
 // which the matrix core works on the scores of tile t+1 and the PV product of
 // tile t-1 while the vector ALUs exponentiate tile t, within the same wave.
 //
-// Decomposition, operand layouts and numerics are those of attn2_kernel
-// (rc_attn2.hip): 128 queries of one (chain, head, key range) per workgroup,
-// 32 per wave; S^T = K Q^T with the permuted key rows; O^T = V^T P^T with the
-// swizzled V^T tile and the ones row that accumulates the softmax
-// denominator; exp2 online softmax with the lazy rescale; uneven key splits
-// and the deterministic combine.  Differences:
+// Operand layouts are those of the cross-attention (rc_attn2.hip): S^T =
+// K Q^T with the permuted key rows; O^T = V^T P^T with the swizzled V^T tile
+// and the ones row that accumulates the softmax denominator.  128 queries of
+// one (chain, head, key range) per workgroup, 32 per wave; exp2 online
+// softmax in which the reference maximum only moves when some query of the
+// wave gained more than 2^8 over it (so the output rescale is rare and the
+// result unchanged); uneven key splits and the deterministic combine.  On
+// top of that:
 //
 // * a four-slot ring: while tile t-1's values and tile t+1's keys are read,
 //   tile t+2 streams in; one barrier per tile;

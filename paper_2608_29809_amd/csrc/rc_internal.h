@@ -70,6 +70,12 @@ struct AttnArgs {
   float scale_log2;      // log2(e)/sqrt(72)
   const void *warm;      // buffer a later kernel reads, warmed into the memory-side cache (or null)
   long long warm_lines;  // 128-byte lines
+  // query projection computed inside the cross-attention (launch_attention2q):
+  // Q = E(Xq . Wq^T + bq), Xq [R][hidden] E, Wq [hidden][hidden] E (row n =
+  // output column n), bq [hidden] fp32; Q above is then unused
+  const void *q_x;
+  const void *q_w;
+  const float *q_b;
 };
 
 template <typename T> hipError_t launch_gemm(const GemmArgs &a, int epi, hipStream_t s);
@@ -101,9 +107,12 @@ hipError_t launch_gemm2_finish(const GemmArgs &a, int epi, const GemmPlan &plan,
                                hipStream_t s, const LnNext *ln = nullptr, bool *ln_done = nullptr);
 template <typename T> hipError_t launch_attention(const AttnArgs &a, int n_chains, int max_rows,
                                                   bool emit_maps, hipStream_t s);
-// bf16 cross-attention to the transposed text values, emitting the
-// delta-column maps when a.pmaps is set (rc_attn2.hip).
-hipError_t launch_attention2(const AttnArgs &a, int n_chains, int max_rows, hipStream_t s);
+// bf16 cross-attention to the transposed text values with its query
+// projection fused in: each workgroup projects its own 64 rows of one head
+// from a.q_x / a.q_w / a.q_b, then attends; emits the delta-column maps when
+// a.pmaps is set (rc_attn2.hip).  hidden 1152, at most 128 keys, one key
+// range.
+hipError_t launch_attention2q(const AttnArgs &a, int n_chains, int max_rows, hipStream_t s);
 // bf16 self-attention with the next tile's score MFMAs overlapping the
 // softmax (rc_attn3.hip); no map emission.
 hipError_t launch_attention3(const AttnArgs &a, int n_chains, int max_rows, hipStream_t s);
