@@ -370,6 +370,14 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
 
   int *rows = (int *)(wsb + wl.rows);
   const int *offsets_dev = dense ? (int *)(wsb + wl.offsets) : act->offsets;
+  // the first chains' row offsets, passed by value to the attention kernels
+  int n_arg_offs = std::min(B, rc::kArgChains), arg_offs[rc::kArgChains + 1];
+  for (int b = 0; b <= n_arg_offs; ++b) arg_offs[b] = dense ? b * N : act->offsets_host[b];
+  auto set_offsets = [&](rc::AttnArgs &a) {
+    a.offsets = offsets_dev;
+    a.n_arg_offs = n_arg_offs;
+    for (int b = 0; b <= n_arg_offs; ++b) a.arg_offs[b] = arg_offs[b];
+  };
   float *X = (float *)(wsb + wl.X);
   void *A1 = wsb + wl.A1, *Q = wsb + wl.Q, *O = wsb + wl.O, *G = wsb + wl.G;
   float *part = (float *)(wsb + wl.part), *ml = (float *)(wsb + wl.ml), *pmaps = (float *)(wsb + wl.pmaps);
@@ -496,7 +504,7 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
     {  // region-level sparse self-attention over the whole slot
       rc::AttnArgs a{};
       a.Q = Q; a.K = Ks; a.V = Vs; a.v_rowmajor = 1; a.chain_stride = slot_chain_stride; a.head_stride = (long long)N * rc::kHeadDim;
-      a.offsets = offsets_dev; a.n_keys = N; a.n_valid = N; a.hidden = C; a.splits = splits;
+      set_offsets(a); a.n_keys = N; a.n_valid = N; a.hidden = C; a.splits = splits;
       a.O = O; a.Opart = part; a.ML = ml; a.total_rows = R; a.scale_log2 = scale_log2;
       if (dense) { a.warm = lw.xq_w; a.warm_lines = wlines(C, C); }
       RC_TRY(timed(c, RC_KC_ATTN_SELF, s, [&] {
@@ -526,7 +534,7 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
       rc::AttnArgs a{};
       a.Q = Q; a.K = tkv; a.V = tkv + (size_t)H * c->Mp * rc::kHeadDim; a.v_rowmajor = 0;
       a.chain_stride = (long long)text_kv_elems_per_entry(c); a.head_stride = (long long)c->Mp * rc::kHeadDim;
-      a.offsets = offsets_dev; a.n_keys = c->Mp; a.n_valid = c->M; a.text_valid = io->text_valid;
+      set_offsets(a); a.n_keys = c->Mp; a.n_valid = c->M; a.text_valid = io->text_valid;
       a.hidden = C; a.splits = 1;
       a.O = O; a.total_rows = R; a.scale_log2 = scale_log2;
       a.q_x = A1; a.q_w = lw.xq_w; a.q_b = lw.xq_b;

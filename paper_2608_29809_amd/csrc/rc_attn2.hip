@@ -106,6 +106,13 @@ __global__ __launch_bounds__(512, 1) void attn2q_kernel(AttnArgs a) {
   const bf16 *Kg = (const bf16 *)a.K + b * a.chain_stride + h * a.head_stride;
   const bf16 *Vg = (const bf16 *)a.V + b * a.chain_stride + h * a.head_stride;  // transposed [72][n_keys]
   if (WARM && wave == 0) warm_lines(a.warm, a.warm_lines, p, T, lds + WARM_OFF);
+  // operands of later phases, fetched now so their latency hides under
+  // phase 1: this thread's bias columns c0 + 8j of the query tile
+  // reduction, and the chain's valid key count
+  float qb[D / 8];
+#pragma unroll
+  for (int j = 0; j < D / 8; ++j) qb[j] = a.q_b[h * D + (tid & 7) + 8 * j];
+  const int nv = a.text_valid ? min(max(a.text_valid[b], 1), a.n_valid) : a.n_valid;
 
   // copies that depend only on (chain, head) go first, in flight while the
   // row offsets are fetched: every text key/value tile, then the first two
@@ -142,7 +149,8 @@ __global__ __launch_bounds__(512, 1) void attn2q_kernel(AttnArgs a) {
   issue_w(0, 0);
   issue_w(1, 1);
 
-  const int r0 = a.offsets[b], r1 = a.offsets[b + 1];
+  const int2 rr = chain_rows(a, b);
+  const int r0 = rr.x, r1 = rr.y;
   const int q0 = r0 + qt * AQ_ROWS;
   if (q0 >= r1) {  // uniform across the workgroup; every copy lands before exit
     wait_vm0();
@@ -237,7 +245,7 @@ __global__ __launch_bounds__(512, 1) void attn2q_kernel(AttnArgs a) {
       const int d = c0 + 8 * j;
       const float v = ((part[q * D + d] + part[(AQ_ROWS + q) * D + d]) + part[(2 * AQ_ROWS + q) * D + d]) +
                       part[(3 * AQ_ROWS + q) * D + d];
-      qs[q * QS_LD + d] = (bf16)(v + a.q_b[h * D + d]);
+      qs[q * QS_LD + d] = (bf16)(v + qb[j]);
     }
     qs[q * QS_LD + D + c0] = (bf16)0.0f;  // columns 72..79
   }
@@ -246,7 +254,6 @@ __global__ __launch_bounds__(512, 1) void attn2q_kernel(AttnArgs a) {
 
   // phase 2: queries 32 qh .., key sub-tile kt
   const int qh = wave & 1, kt = wave >> 1;
-  const int nv = a.text_valid ? min(max(a.text_valid[b], 1), a.n_valid) : a.n_valid;
   const float c2 = a.scale_log2;
   float *ml = (float *)(lds + ML_OFF);
   float *sd = (float *)(lds + SD_OFF);

@@ -46,6 +46,8 @@ struct GemmArgs {
   long long warm_lines;  // 128-byte lines
 };
 
+constexpr int kArgChains = 16;  // chains whose row offsets travel in the kernel arguments
+
 struct AttnArgs {
   const void *Q;         // [R][C] E compact queries (chains concatenated)
   const void *K;         // chain 0, head 0 keys [n_keys][72]
@@ -76,7 +78,18 @@ struct AttnArgs {
   const void *q_x;
   const void *q_w;
   const float *q_b;
+  // offsets[0..n_arg_offs] by value (the host's copy): chains b < n_arg_offs
+  // read their row range from the kernel arguments, one dependent load less
+  // at kernel start, when every cache line is cold
+  int n_arg_offs;
+  int arg_offs[kArgChains + 1];
 };
+
+// Row range [first, last) of chain b.
+__device__ __forceinline__ int2 chain_rows(const AttnArgs &a, int b) {
+  if (b < a.n_arg_offs) return make_int2(a.arg_offs[b], a.arg_offs[b + 1]);
+  return make_int2(a.offsets[b], a.offsets[b + 1]);
+}
 
 template <typename T> hipError_t launch_gemm(const GemmArgs &a, int epi, hipStream_t s);
 
