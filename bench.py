@@ -192,6 +192,19 @@ def main():
     log("per-step kernel time by class: " + ", ".join(f"{k} {v['total_ms']:.3f}ms/{v['launches']}"
                                                       for k, v in sorted(per.items(), key=lambda kv: -kv[1]['total_ms'])))
 
+    # the dense step's kernel classes, for the vendor comparison below
+    model.set_kernel_timing(True)
+    for k in range(4):
+        dense(k)
+    torch.cuda.synchronize()
+    per_dense = {}
+    for c, name in enumerate(abi.KERNEL_CLASSES):
+        ms, n = model.kernel_timing(c)
+        if n:
+            per_dense[name] = dict(total_ms=ms / 4, launches=n // 4, avg_us=1000.0 * ms / n)
+    model.set_kernel_timing(False)
+    vendor = None if args.quick else vendor_leg(shape, R, per, per_dense, ms_reuse, ms_dense)
+
     C, N, F, M = shape.hidden, shape.tokens, shape.mlp, shape.text_len
     work = class_work(shape, R, 1)
     by_class = {}
@@ -288,6 +301,7 @@ def main():
         "dense_step_ms": round(ms_dense, 4),
         "dense_steps_per_s": round(1000.0 / ms_dense, 3),
         "speedup_vs_dense": round(ms_dense / ms_reuse, 3),
+        "vendor_gemm_reference": vendor,
         "schedule": schedule,
         "kernels_ms_per_step": {k: round(v["total_ms"], 4) for k, v in per.items()},
         "roofline": roofline,
@@ -299,6 +313,51 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def vendor_leg(shape, R, per, per_dense, ms_reuse, ms_dense):
+    """Each GEMM class of the step timed beside the vendor's bf16 GEMM
+    (torch.mm, served by hipBLASLt) on the same shape, at the region step's R
+    rows and the dense step's N rows.  The dense step is then also stated as
+    if every one of its GEMMs ran at the faster of the two, and the reuse
+    step's speedup against that step: a check on the dense denominator, not
+    part of the path (the library runs its own kernels only)."""
+    import torch
+    C, N, F = shape.hidden, shape.tokens, shape.mlp
+    shapes = {"gemm_qkv": (3 * C, C), "gemm_proj": (C, C), "gemm_xproj": (C, C), "gemm_fc1": (F, C),
+              "gemm_fc2": (C, F)}
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def mm_us(m, n, k):
+        a = torch.randn(m, k, device="cuda", dtype=torch.bfloat16)
+        b = torch.randn(k, n, device="cuda", dtype=torch.bfloat16).contiguous()
+        for _ in range(3):
+            torch.mm(a, b)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(20):
+            torch.mm(a, b)
+        e1.record()
+        torch.cuda.synchronize()
+        return 1000.0 * e0.elapsed_time(e1) / 20
+
+    out = {"rows": {"region": R, "dense": N}, "classes": {}}
+    saved_us = 0.0
+    for cls, (n, k) in shapes.items():
+        row = {}
+        for tag, m, table in (("region", R, per), ("dense", N, per_dense)):
+            v = mm_us(m, n, k)
+            ours = table.get(cls, {}).get("avg_us")
+            row[tag] = dict(ours_us=round(ours, 2) if ours else None, vendor_us=round(v, 2))
+            if tag == "dense" and ours:
+                saved_us += max(0.0, ours - v) * table[cls]["launches"]
+        out["classes"][cls] = row
+    dense_best = ms_dense - saved_us / 1000.0
+    out["dense_step_ms_at_faster_gemms"] = round(dense_best, 4)
+    out["speedup_vs_that_dense_step"] = round(dense_best / ms_reuse, 3)
+    log(f"vendor GEMM check: dense step at the faster GEMM of each class {dense_best:.3f} ms "
+        f"(ours {ms_dense:.3f}); reuse speedup against it {dense_best / ms_reuse:.2f}x")
+    return out
 
 
 def hosted_leg(model, shape, cache, act, lat1, tgrid, tkv1, s_from, ms_device, R):
