@@ -116,7 +116,7 @@ constexpr int kMaxSplits = 8;
 int part_cap_rows(int max_rows) { return kMaxSplits * std::min(max_rows, 1024); }
 
 struct WsLayout {
-  size_t rows, offsets, X, A1, Q, O, G, part, ml, pmaps, e, th, temb, t0, gpart, total;
+  size_t rows, offsets, X, A1, Q, O, G, part, ml, pmaps, e, th, temb, t0, gpart, fstats, fextra, total;
   size_t gpart_floats;
   size_t txt_h, txt_y, txt_total;
 };
@@ -143,6 +143,8 @@ WsLayout ws_layout(const rc_ctx *c, int max_rows, int B) {
   w.t0 = take((size_t)6 * c->C * 4);
   w.gpart_floats = (size_t)std::min(max_rows, 2048) * 8 * c->C;
   w.gpart = take(w.gpart_floats * 4);
+  w.fstats = take(R * rc::kFoldMaxTiles * 8 + 256);  // + the 16-byte reads' overhang
+  w.fextra = take((size_t)4 * c->C * c->esz);
   w.total = o;
   // text preparation reuses the front of the workspace
   size_t t = 0;
@@ -385,6 +387,20 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
   float *t0 = (float *)(wsb + wl.t0);
   float *gpart = (float *)(wsb + wl.gpart);
   const size_t gpf = wl.gpart_floats;
+  float2 *fstats = (float2 *)(wsb + wl.fstats);
+  void *fextra = wsb + wl.fextra;
+  // bf16: the MLP-up LayerNorm folds into the GEMMs on either side of it
+  // when both run unsplit.  The cross out-projection's epilogue writes each
+  // row's mean and sum of squared deviations over its column tile and the
+  // modulated copy x~ = x (1 + scale); the MLP-up GEMM takes four more A rows
+  // per tile, (1 + scale) and shift as bf16 pairs, and applies
+  // h W^T = r (x~ W^T - mean u) + v after its K loop (u, v: the products of
+  // those rows).
+  int fold_nt = 0;
+  if (sizeof(T) == 2) {
+    const rc::GemmPlan px = rc::plan_gemm2(R, C, C, gpf), p1 = rc::plan_gemm2(R, F, C, gpf);
+    if (px.splits == 1 && p1.splits == 1 && C % px.bn == 0 && C / px.bn <= rc::kFoldMaxTiles) fold_nt = C / px.bn;
+  }
 
   if (dense) RC_TRY(timed(c, RC_KC_MISC, s, [&] { return rc::launch_dense_offsets((int *)offsets_dev, B, N, s); }));
   RC_TRY(timed(c, RC_KC_MISC, s, [&] {
@@ -554,20 +570,28 @@ rc_status run_step(rc_ctx *c, const rc_cache_view *cache, int step, const rc_ste
           return rc::launch_maps_reduce(pmaps, rows, io->maps, R, H, io->n_delta, N, s);
         }));
     }
-    {  // cross out-projection + residual (no gate)
+    {  // cross out-projection + residual (no gate); the fold's statistics and x~
       rc::GemmArgs g{};
       g.A = O; g.W = lw.xproj_w; g.bias = lw.xproj_b; g.M = R; g.N = C; g.K = C; g.lda = C;
       g.X = X; g.ldx = C;
+      if (fold_nt) {
+        g.xt = A1;
+        g.fold_scale[0] = lw.sst + 4 * C; g.fold_scale[1] = t0 + 4 * C;
+        g.fold_shift[0] = lw.sst + 3 * C; g.fold_shift[1] = t0 + 3 * C;
+        g.fold_stats = fstats; g.fold_nt = fold_nt; g.fold_extra = fextra;
+      }
       if (!dense) { g.warm = (const char *)lw.fc2_w + fc2_half * 128; g.warm_lines = fc2_lines - fc2_half; }
       else { g.warm = lw.fc2_w; g.warm_lines = fc2_lines; }
       RC_TRY(gemm<T>(c, RC_KC_GEMM_XPROJ, g, rc::EPI_RESID, gpart, gpf, s));
     }
-    RC_TRY(timed(c, RC_KC_NORM, s, [&] { return rc::launch_ln_mod<T>(X, R, C, lw.sst, t0, 3, c->cfg.ln_eps, A1, s); }));
+    if (!fold_nt)
+      RC_TRY(timed(c, RC_KC_NORM, s, [&] { return rc::launch_ln_mod<T>(X, R, C, lw.sst, t0, 3, c->cfg.ln_eps, A1, s); }));
     {  // MLP up + GELU
       rc::GemmArgs g{};
       g.A = A1; g.W = lw.fc1_w; g.bias = lw.fc1_b; g.M = R; g.N = F; g.K = C; g.lda = C; g.out = G; g.ldo = F;
       if (dense && l + 1 < L) { g.warm = c->layers[l + 1].qkv_w; g.warm_lines = wlines(3 * C, C); }
-      RC_TRY(gemm<T>(c, RC_KC_GEMM_FC1, g, rc::EPI_GELU, gpart, gpf, s));
+      if (fold_nt) { g.fold_stats = fstats; g.fold_nt = fold_nt; g.fold_extra = fextra; g.fold_eps = c->cfg.ln_eps; }
+      RC_TRY(gemm<T>(c, RC_KC_GEMM_FC1, g, fold_nt ? rc::EPI_GELU_FOLD : rc::EPI_GELU, gpart, gpf, s));
     }
     {  // MLP down + gate + residual; merge into the cached hidden state
       rc::GemmArgs g{};

@@ -13,6 +13,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
+constexpr int kLdsBytes = 160 * 1024;  // LDS per CU
 constexpr int kHeadDim = 72;
 
 // Matrix-core traits per storage type.  Both use the 32x32 output block whose
@@ -55,6 +56,20 @@ template <> __device__ __forceinline__ bf16 from_f<bf16>(float v) { return (bf16
 
 // 16-byte vector of storage elements
 struct alignas(16) V16 { uint32_t w[4]; };
+
+// Sum over the 16 lanes of a DPP row, in the vector ALU (no LDS permute):
+// neighbours, pairs, half-row mirror, row mirror.  Every step combines two
+// partial results that both lanes of a pair hold bit for bit, so all 16
+// lanes end with the same value.
+template <int CTRL> __device__ __forceinline__ float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_mov<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_mov<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_mov<0x141>(v);  // row_half_mirror
+  return v + dpp_mov<0x140>(v);  // row_mirror
+}
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

@@ -51,7 +51,7 @@ __device__ __forceinline__ void epi_store(const GemmArgs &g, int m, int n, float
                                           int dd) {
   if (EPI == EPI_STORE) {
     ((bf16 *)g.out)[(size_t)m * g.ldo + n] = (bf16)v;
-  } else if (EPI == EPI_GELU) {
+  } else if (EPI == EPI_GELU || EPI == EPI_GELU_FOLD) {
     ((bf16 *)g.out)[(size_t)m * g.ldo + n] = (bf16)gelu_tanh(v);
   } else if (EPI == EPI_RESID) {
     float *xp = g.X + (size_t)m * g.ldx + n;
@@ -123,7 +123,7 @@ template <int EPI>
 __device__ __forceinline__ void epi4(const GemmArgs &g, int m, int n, float *v, int part) {
   if (EPI == EPI_STORE) {
     st4((bf16 *)g.out + (size_t)m * g.ldo + n, v);
-  } else if (EPI == EPI_GELU) {
+  } else if (EPI == EPI_GELU || EPI == EPI_GELU_FOLD) {
     float w[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) w[q] = gelu_tanh(v[q]);
@@ -163,6 +163,28 @@ __device__ __forceinline__ void col_info(const GemmArgs &g, int n, float &bn, fl
   }
 }
 
+constexpr int pow2_ceil(int v) { return v <= 1 ? 1 : 2 * pow2_ceil((v + 1) / 2); }
+
+// Sum over W = 2, 4, 8 or 16 consecutive lanes (aligned groups), in DPP;
+// every lane of a group ends with the same value.
+template <int W> __device__ __forceinline__ float lane_group_sum(float v) {
+  static_assert(W == 2 || W == 4 || W == 8 || W == 16, "2 to 16 lanes");
+  if (W == 16) return row16_sum(v);
+  v += dpp_mov<0xB1>(v);                  // quad_perm [1,0,3,2]
+  if (W >= 4) v += dpp_mov<0x4E>(v);      // quad_perm [2,3,0,1]
+  if (W >= 8) v += dpp_mov<0x141>(v);     // row_half_mirror
+  return v;
+}
+
+// Sum over W = 16 or 32 consecutive lanes (aligned groups): DPP within each
+// row of 16, then a swizzle exchanging the two rows of a 32-lane half.
+template <int W> __device__ __forceinline__ float group_sum(float v) {
+  static_assert(W == 16 || W == 32, "16- or 32-lane groups");
+  v = row16_sum(v);
+  if (W == 32) v += __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x401F));  // lane ^ 16
+  return v;
+}
+
 template <int BM, int BN, int STAGES, int KG, int WGM, int WGN, int EPI, bool SPLIT>
 __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, float *partial, int k_per_split) {
   constexpr int NW = WGM * WGN;                       // waves per K group
@@ -178,7 +200,24 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
   constexpr int PASSES = (BM * CLD * 4 <= GROUP_BYTES) ? 1 : 2;
   constexpr int HB = BM / PASSES;
   static_assert(HB * CLD * 4 <= GROUP_BYTES && HB % WM == 0, "an output band must fit a group's ring");
-  __shared__ __attribute__((aligned(1024))) char lds[KG * GROUP_BYTES + 256];
+  // folded LayerNorm (EPI_GELU_FOLD): a tile's last four A rows are the
+  // fold's (1 + scale) and shift rows, each as a bf16 pair (high part, then
+  // the rounding remainder), so it covers TROWS rows of the output
+  constexpr bool FOLD = EPI == EPI_GELU_FOLD;
+  constexpr int TROWS = FOLD ? BM - 4 : BM;
+  // after the rings: [BM] (mean, r) per row, [KG][2][BN] u and v partials;
+  // the producer's statistics of the tile's rows [TROWS][fold_nt] get a
+  // region of their own where that keeps the workgroups per CU (merged after
+  // the K loop, their loads land during it), else they pass through the
+  // first ring's last stage, which the prologue leaves empty (merged before
+  // the K loop)
+  constexpr int FOLD_OFF = KG * GROUP_BYTES + 256;
+  constexpr int LDS_BASE = FOLD_OFF + (FOLD ? BM * 8 + KG * 2 * BN * 4 : 0);
+  constexpr int ST_BYTES = TROWS * kFoldMaxTiles * 8;
+  constexpr bool ST_OWN = FOLD && kLdsBytes / (LDS_BASE + ST_BYTES) == kLdsBytes / LDS_BASE;
+  constexpr int FOLD_ST_OFF = ST_OWN ? LDS_BASE : (STAGES - 1) * STAGE_BYTES;
+  static_assert(!FOLD || ST_OWN || ST_BYTES <= STAGE_BYTES, "the statistics must fit a stage");
+  __shared__ __attribute__((aligned(1024))) char lds[LDS_BASE + (ST_OWN ? ST_BYTES : 0)];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int kgrp = wave / NW, w4 = wave % NW;
@@ -197,7 +236,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
   constexpr int GM = 16;
   const int grp = r / (GM * tiles_n), gm = min(GM, tiles_m - grp * GM), idx = r - grp * GM * tiles_n;
   const int tm = grp * GM + idx % gm, tn = idx / gm;
-  const int m0 = tm * BM, n0 = tn * BN;
+  const int m0 = tm * TROWS, n0 = tn * BN;
   // K group kgrp covers its own contiguous share of this split's K range
   if (wave == 0) warm_lines(g.warm, g.warm_lines, p, T, lds + KG * GROUP_BYTES);
   const int kps_g = k_per_split / KG;
@@ -217,6 +256,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
       const int r = ch >> 3, c = (ch & 7) ^ swz(r);
       const int gr = min(m0 + r, g.M - 1);
       const bf16 *src = A + (size_t)gr * g.lda + k0 + c * 8;
+      if (FOLD && r >= TROWS) src = (const bf16 *)g.fold_extra + (size_t)(r - TROWS) * g.K + k0 + c * 8;
       __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
                                        (__attribute__((address_space(3))) void *)(sa + (i * NW + w4) * 1024), 16, 0, 0);
     }
@@ -238,9 +278,64 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
+  // the fold's per-row partial statistics of the tile's rows (contiguous:
+  // TROWS x fold_nt pairs) go to LDS by direct loads issued before the first
+  // stages; each wave loads and merges the statistics of its own FRW rows,
+  // so it waits for its own loads only (they are older than its stage
+  // loads) and needs no barrier
+  constexpr int NTH = 64 * NW * KG, NWAVES = NW * KG;
+  constexpr int FRW = pow2_ceil((TROWS + NWAVES - 1) / NWAVES);  // rows per wave
+  constexpr int FLR = 64 / FRW;                                  // lanes per row
+  static_assert(!FOLD || (FLR >= 2 && FLR <= 16), "2 to 16 lanes per row");
+  const float2 *sts = (const float2 *)(lds + FOLD_ST_OFF);
+  float2 *fold_rs = (float2 *)(lds + FOLD_OFF);        // [BM] (mean, r)
+  float *fold_uv = (float *)(lds + FOLD_OFF + BM * 8);  // [KG][2][BN]
+  const int frow0 = wave * FRW;  // the wave's first row (FRW and m0 even: 16-byte aligned)
+  if (FOLD && frow0 < TROWS) {
+    const int nt = g.fold_nt, nch = min(FRW, TROWS - frow0) * nt / 2;
+    const int first = (m0 + frow0) * nt / 2, last = (g.M * nt + 1) / 2 - 1;
+    for (int c0 = 0; c0 < nch; c0 += 64) {
+      if (c0 + lane < nch) {
+        const char *src = (const char *)g.fold_stats + (size_t)min(first + c0 + lane, last) * 16;
+        __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)src,
+                                         (__attribute__((address_space(3))) void *)(lds + FOLD_ST_OFF + (frow0 * nt / 2 + c0) * 16),
+                                         16, 0, 0);
+      }
+    }
+  }
+
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s)
     if (s < nk) issue(s, kbeg + s * G2_BK);
+  // FLR lanes per row merge the row's equal-size partials (strided over the
+  // lanes, then summed across them: a fixed order)
+  auto fold_merge = [&]() {
+    const int nt = g.fold_nt, row = frow0 + lane / FLR, j0 = lane % FLR;
+    const float2 *st = sts + min(row, TROWS - 1) * nt;
+    constexpr int PER = (kFoldMaxTiles + FLR - 1) / FLR;
+    float2 p[PER];  // (unpredicated reads: no branch between them)
+#pragma unroll
+    for (int i = 0; i < PER; ++i) p[i] = st[min(j0 + i * FLR, nt - 1)];
+    float sm = 0.0f;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) sm += j0 + i * FLR < nt ? p[i].x : 0.0f;
+    const float mu = lane_group_sum<FLR>(sm) / (float)nt;
+    const float cnt = (float)(g.K / nt);
+    float m2 = 0.0f;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const float d = p[i].x - mu;
+      m2 += j0 + i * FLR < nt ? p[i].y + cnt * d * d : 0.0f;
+    }
+    m2 = lane_group_sum<FLR>(m2);
+    if (j0 == 0 && row < TROWS) fold_rs[row] = make_float2(mu, rsqrtf(m2 / (float)g.K + g.fold_eps));
+  };
+  if (FOLD && !ST_OWN && frow0 < TROWS) {
+    // the wave's own statistics are older than its stage loads
+    if (nk >= STAGES - 1) wait_vmcnt<(STAGES - 1) * LPS>();
+    else wait_vmcnt<0>();
+    fold_merge();
+  }
 
   const int g32 = lane >> 5, r32 = lane & 31;
   for (int kt = 0; kt < nk; ++kt) {
@@ -286,6 +381,22 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
   // group order while the band is written back with 16-byte row-contiguous
   // accesses.  Tiles of transposed text values are walked column-major
   // instead so that consecutive threads write consecutive tokens.
+  if (FOLD) {
+    if (ST_OWN && frow0 < TROWS) {  // (every load has completed: the loop's last wait)
+      wait_vmcnt<0>();
+      fold_merge();
+    }
+    // rows BM-4 .. BM-1 (u as two parts, then v): local rows 28 to 31 of
+    // the last 32-row block, accumulators 12 to 15 of the upper half-wave
+    if (wm == WGM - 1 && g32 == 1) {
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int col = wn * WN + j * 32 + r32;
+        fold_uv[(kgrp * 2) * BN + col] = acc[FM - 1][j][12] + acc[FM - 1][j][13];
+        fold_uv[(kgrp * 2 + 1) * BN + col] = acc[FM - 1][j][14] + acc[FM - 1][j][15];
+      }
+    }
+  }
   float *ct = (float *)ring;
   auto tile_at = [&](int row, int col) {
     float v = 0.0f;
@@ -293,7 +404,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
     for (int q = 0; q < KG; ++q) v += ((const float *)(lds + q * GROUP_BYTES))[row * CLD + col];
     return v;
   };
-  constexpr int NT = 64 * NW * KG;
+  constexpr int NT = NTH;
   const int tile_part = (EPI == EPI_QKV || EPI == EPI_TEXTKV) ? n0 / g.hidden : 0;
   const bool transposed = EPI == EPI_TEXTKV && tile_part == 1;
 #pragma unroll
@@ -333,10 +444,35 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
       const f32x4 bb = g.bias ? *(const f32x4 *)(g.bias + n) : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
       constexpr bool NEED_X = EPI == EPI_RESID;
       const bool need_rows = (EPI == EPI_RESID && g.hslot) || (EPI == EPI_QKV && tile_part > 0);
-      f32x4 gt = f32x4{1.0f, 1.0f, 1.0f, 1.0f};
-      if (EPI == EPI_RESID && g.gate) {
-        gt = *(const f32x4 *)(g.gate + n);
-        if (g.gate2) gt += *(const f32x4 *)(g.gate2 + n);
+      // column loads land in registers with their defaults and are combined
+      // only after the row loads below are issued (a use inside a branch
+      // would make the row loads wait for them)
+      f32x4 ga = f32x4{1.0f, 1.0f, 1.0f, 1.0f}, gb = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+      if (EPI == EPI_RESID && g.gate) ga = *(const f32x4 *)(g.gate + n);
+      if (EPI == EPI_RESID && g.gate && g.gate2) gb = *(const f32x4 *)(g.gate2 + n);
+      // fold consumer: u and v of the tile's columns, summed over the K groups
+      f32x4 fu = f32x4{0.0f, 0.0f, 0.0f, 0.0f}, fw = fu;
+      if (FOLD) {
+#pragma unroll
+        for (int k = 0; k < KG; ++k) {
+          fu += *(const f32x4 *)(fold_uv + (k * 2) * BN + c4);
+          fw += *(const f32x4 *)(fold_uv + (k * 2 + 1) * BN + c4);
+        }
+      }
+      // fold producer: the next LayerNorm's (1 + scale), and the consumer's
+      // four extra rows (1 + scale and shift, each split into a bf16 high
+      // part and its remainder so that u and v carry ~16 bits: a rounding of
+      // these per-column factors would be the same for every row)
+      // (unconditional loads, from X's first row without the fold: a branch
+      // here would take the add of 1 into it, and the wait with it)
+      const bool fold_out = EPI == EPI_RESID && g.fold_stats;
+      const bool fold_rows = fold_out && tm == 0 && row0 == 0;  // writes the consumer's extra rows
+      f32x4 fa = f32x4{0.0f, 0.0f, 0.0f, 0.0f}, fb = fa, fc = fa, fd = fa;
+      if (EPI == EPI_RESID) {
+        fa = *(const f32x4 *)((fold_out ? g.fold_scale[0] : g.X) + n);
+        fb = *(const f32x4 *)((fold_out ? g.fold_scale[1] : g.X) + n);
+        fc = *(const f32x4 *)((fold_rows ? g.fold_shift[0] : g.X) + n);
+        fd = *(const f32x4 *)((fold_rows ? g.fold_shift[1] : g.X) + n);
       }
       f32x4 xo[NEED_X ? IT : 1];
       int pk[IT];
@@ -346,14 +482,21 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
         if (NEED_X) xo[it] = *(const f32x4 *)(g.X + (size_t)m * g.ldx + n);
         pk[it] = need_rows ? g.rows[m] : 0;
       }
+      const f32x4 gt = ga + gb, fsc = 1.0f + fa + fb;
 #pragma unroll
       for (int it = 0; it < IT; ++it) {
         const int row = row0 + it * RPI;
         const int m = m0 + rb + row;
-        if ((IT * RPI != HB && row >= HB) || m >= g.M) continue;
+        if ((IT * RPI != HB && row >= HB) || m >= g.M || (FOLD && rb + row >= TROWS)) continue;
         float v[4];
+        if (FOLD) {  // h W^T + b = r (x~ W^T - mean u) + v + b
+          const float2 st = fold_rs[rb + row];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) v[q] = tile_at(row, c4 + q) + bb[q];
+          for (int q = 0; q < 4; ++q) v[q] = st.y * (tile_at(row, c4 + q) - st.x * fu[q]) + fw[q] + bb[q];
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) v[q] = tile_at(row, c4 + q) + bb[q];
+        }
         if (EPI == EPI_RESID) {
           f32x4 x;
 #pragma unroll
@@ -362,7 +505,20 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
             v[q] = x[q];
           }
           *(f32x4 *)(g.X + (size_t)m * g.ldx + n) = x;
-          if (g.xt) st4((bf16 *)g.xt + (size_t)m * g.ldx + n, v);
+          if (fold_out) {
+            // the next LayerNorm's statistics of this row over the tile's
+            // BN columns (every lane of the row's group takes part), and x~
+            const float mean = group_sum<BN / 4>((v[0] + v[1]) + (v[2] + v[3])) / BN;
+            float d2 = 0.0f;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) d2 += (v[q] - mean) * (v[q] - mean);
+            d2 = group_sum<BN / 4>(d2);
+            if (c4 == 0) g.fold_stats[(size_t)m * g.fold_nt + n0 / BN] = make_float2(mean, d2);
+            const float xs[4] = {v[0] * fsc[0], v[1] * fsc[1], v[2] * fsc[2], v[3] * fsc[3]};
+            st4((bf16 *)g.xt + (size_t)m * g.ldx + n, xs);
+          } else if (g.xt) {
+            st4((bf16 *)g.xt + (size_t)m * g.ldx + n, v);
+          }
           if (g.hrows) st4((bf16 *)g.hrows + (size_t)m * g.N + n, v);
           if (g.hslot)
             st4((bf16 *)g.hslot + row_chain(pk[it]) * g.chain_stride + (size_t)row_token(pk[it]) * g.hidden + n, v);
@@ -373,6 +529,21 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void gemm2_kernel(GemmArgs g, 
         } else {
           epi4<EPI>(g, m, n, v, tile_part);
         }
+      }
+      // (after the rows: a branch between the loads above and their use
+      // would make the residual loads wait for the scale loads)
+      if (fold_rows && pass == 0) {
+        const f32x4 fsh = fc + fd;
+        float part[4][4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          part[0][q] = (float)(bf16)fsc[q];
+          part[1][q] = fsc[q] - part[0][q];
+          part[2][q] = (float)(bf16)fsh[q];
+          part[3][q] = fsh[q] - part[2][q];
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) st4((bf16 *)g.fold_extra + (size_t)e * g.N + n, part[e]);
       }
     } else {
       // a wave walks one column, lanes on consecutive rows: each store covers
@@ -487,7 +658,8 @@ __global__ __launch_bounds__(256) void splitk_finish_ln_kernel(GemmArgs g, const
 
 template <int BM, int BN, int STAGES, int KG, int WGM, int WGN, bool SPLIT>
 static void launch_g2(const GemmArgs &a, int epi, int splits, float *partial, hipStream_t s) {
-  dim3 grid(a.N / BN, (a.M + BM - 1) / BM, splits);
+  const int trows = epi == EPI_GELU_FOLD ? BM - 4 : BM;
+  dim3 grid(a.N / BN, (a.M + trows - 1) / trows, splits);
   const int kps = a.K / splits;
 #define RC_G2(E)                                                                                       \
   rc_launch(gemm2_kernel<BM, BN, STAGES, KG, WGM, WGN, E, SPLIT>, grid, dim3(64 * WGM * WGN * KG), 0, s, \
@@ -495,6 +667,9 @@ static void launch_g2(const GemmArgs &a, int epi, int splits, float *partial, hi
   switch (epi) {
     case EPI_STORE: RC_G2(EPI_STORE); break;
     case EPI_GELU: RC_G2(EPI_GELU); break;
+    case EPI_GELU_FOLD:
+      if constexpr (!SPLIT) RC_G2(EPI_GELU_FOLD);
+      break;
     case EPI_RESID: RC_G2(EPI_RESID); break;
     case EPI_QKV: RC_G2(EPI_QKV); break;
     case EPI_TEXTKV: RC_G2(EPI_TEXTKV); break;
@@ -590,6 +765,14 @@ hipError_t launch_gemm2(const GemmArgs &a, int epi, const GemmPlan &pl, float *p
   if (a.M <= 0) return hipSuccess;
   if ((pl.bn != 128 && pl.bn != 64) || a.N % pl.bn || a.K % (G2_BK * pl.splits * pl.kg)) return hipErrorInvalidValue;
   const bool split = pl.splits > 1;
+  // the folded LayerNorm needs the whole K range in one launch and the
+  // producer's per-tile statistics (equal column counts, at most kFoldMaxTiles)
+  if (epi == EPI_GELU_FOLD &&
+      (split || a.fold_nt <= 0 || a.fold_nt > kFoldMaxTiles || a.K % a.fold_nt || !a.fold_stats || !a.fold_extra))
+    return hipErrorInvalidValue;
+  // the fold's producer writes its statistics from the one-pass row epilogue
+  if (epi == EPI_RESID && a.fold_stats && (split || a.fold_nt != a.N / pl.bn || !a.xt || !a.fold_extra))
+    return hipErrorInvalidValue;
   // 4-wave K groups: 128 rows = 2x2 waves of 64x64, 64 rows = 2x2 of 32x64,
   // 32 rows = 1x4 of 32x32, 64x64 tiles = 2x2 of 32x32; 8-wave: 128 rows =
   // 4x2 of 32x64 or 2x4 of 64x32, 64 rows = 2x4 of 32x32

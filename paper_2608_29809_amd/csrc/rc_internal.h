@@ -12,6 +12,9 @@ enum GemmEpi {
   EPI_RESID = 2,   // X += gate * (acc + bias); optional E copies of X (xt, H slot scatter, hidden rows)
   EPI_QKV = 3,     // q -> out (compact), k -> K slot, v -> V slot (token-major rows, like K)
   EPI_TEXTKV = 4,  // text keys/values -> per-chain text K / transposed V
+  // out = E(gelu_tanh(r (acc - mu u) + v + bias)): a LayerNorm + modulation of
+  // the A rows folded into the GEMM (see GemmArgs::fold_*)
+  EPI_GELU_FOLD = 5,
 };
 
 struct GemmArgs {
@@ -44,7 +47,27 @@ struct GemmArgs {
   // buffer a later kernel reads, warmed into the memory-side cache (or null)
   const void *warm;
   long long warm_lines;  // 128-byte lines
+  // LayerNorm + modulation folded into the next GEMM.  With h = (x - mu) r
+  // (1 + scale) + shift (r = 1/sqrt(var + eps) over the row), h W^T =
+  // r (x~ W^T - mu u) + v, where x~ = x (1 + scale), u = W (1 + scale) and
+  // v = W shift.  Producer (EPI_RESID, fold_stats set): xt receives E(x~)
+  // instead of E(x); per row and BN-column tile, the mean and the sum of
+  // squared deviations of the updated x go to fold_stats[m * fold_nt + tile];
+  // the workgroups of row tile 0 write 1 + scale and shift into fold_extra,
+  // each as two rows: its bf16 rounding, then the bf16 rounding of the
+  // remainder.  Consumer (EPI_GELU_FOLD): a BM-row tile holds BM - 4 rows of
+  // A (= x~) and fold_extra's four rows, whose products summed in pairs are
+  // u and v; fold_stats is merged per row (in tile order) into mu and r.
+  const float *fold_scale[2];  // scale = fold_scale[0] + fold_scale[1], [N] each (producer)
+  const float *fold_shift[2];  // shift = fold_shift[0] + fold_shift[1] (producer)
+  float2 *fold_stats;          // [M][fold_nt] (mean, sum of squared deviations)
+  int fold_nt;                 // producer column tiles (K / fold_nt columns each)
+  void *fold_extra;            // [4][C] E
+  float fold_eps;              // consumer
 };
+// most producer column tiles a folded LayerNorm merges per row
+constexpr int kFoldMaxTiles = 24;
+
 
 constexpr int kArgChains = 16;  // chains whose row offsets travel in the kernel arguments
 

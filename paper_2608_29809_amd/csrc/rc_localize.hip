@@ -13,13 +13,7 @@ namespace rc {
 constexpr int LG_TOK = 16;  // tokens per workgroup, 4 per wave
 constexpr int LG_HC = 4;    // heads whose rows a wave loads at once
 
-// Max and sum over the 16 lanes of a DPP row, in the vector ALU (no LDS
-// permute): neighbours, pairs, half-row mirror, row mirror.  Every step
-// combines two partial results that both lanes of a pair hold bit for bit,
-// so all 16 lanes end with the same value.
-template <int CTRL> __device__ __forceinline__ float dpp_mov(float v) {
-  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
-}
+// Max over the 16 lanes of a DPP row (the steps of row16_sum).
 // IEEE maximum (NaN-propagating): one v_maximum3/v_maximum on gfx950, with
 // no operand canonicalisation as fmaxf needs.
 __device__ __forceinline__ float fmax_(float a, float b) { return __builtin_elementwise_maximum(a, b); }
@@ -28,12 +22,6 @@ __device__ __forceinline__ float row16_max(float v) {
   v = fmax_(v, dpp_mov<0x4E>(v));   // quad_perm [2,3,0,1]
   v = fmax_(v, dpp_mov<0x141>(v));  // row_half_mirror
   return fmax_(v, dpp_mov<0x140>(v));  // row_mirror
-}
-__device__ __forceinline__ float row16_sum(float v) {
-  v += dpp_mov<0xB1>(v);
-  v += dpp_mov<0x4E>(v);
-  v += dpp_mov<0x141>(v);
-  return v + dpp_mov<0x140>(v);
 }
 
 // partial[l][tok][j] = sum_h softmax(Z[l][h][tok][:])[delta_j].  One

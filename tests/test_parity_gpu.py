@@ -211,6 +211,8 @@ def _check_teacher_forced(shape, got, per_chain_idx, ctx):
         w = summarize(per)
         _say(f"chain {b} R={idx.size} per block (re-synchronised), worst: " +
              " ".join(f"{k} {v:.2e}" for k, v in w.items()))
+        _say(f"chain {b} per block, median: " +
+             " ".join(f"{k} {np.median([e[k] for e in per]):.2e}" for k in ("H", "dH", "K", "V")))
         bad = gate_failures(per, tl)
         assert not bad, (b, bad[:3])
 
