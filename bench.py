@@ -277,6 +277,8 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(shape, W, idx, args)
+        if not args.quick:
+            cpu["by_config"] = cpu_baseline_configs(shape, W, args)
 
     value = args.steps / t_reuse
     out = {
@@ -723,6 +725,71 @@ def cpu_baseline(shape, W, idx, args):
                        f"float32 NumPy",
                 sample_seconds=round(dt, 3), nproc=len(os.sched_getaffinity(0)), cpu_model=_cpu_model(),
                 blas=blas)
+
+
+def cpu_baseline_configs(shape, W, args):
+    """The oracle (float32, host cores) on the other workloads the GPU legs
+    time, each on a bounded sample scaled to the whole: the 512 px region
+    step of the resolution sweep (all blocks) and its dense step (first 4
+    blocks), the 1024 px dense step (first block) and the 1024 px
+    localisation read-out (4 of the 28 layers of logits, same per-layer shape
+    and distribution as the GPU leg's)."""
+    import dataclasses
+    import oracle as O
+    import synth
+    f32 = np.float32
+    L = shape.layers
+
+    def first_blocks(sh, n):
+        n = max(1, min(n, sh.layers))
+        Wn = dict(W)
+        Wn["layers"] = W["layers"][:n]
+        return dataclasses.replace(sh, layers=n), Wn, n
+
+    def text_kv(sh, Wn, seed):
+        y = O.caption_projection(Wn, synth.make_text(sh, 1, seed)[0], dt=f32)
+        return [O.text_kv(lw, y, sh.heads, dt=f32) for lw in Wn["layers"]]
+
+    out = {}
+    # 512 px: the resolution sweep's 15 % blob region
+    s2 = dataclasses.replace(shape, grid_h=32, grid_w=32)
+    idx2 = synth.resolution_region(args.seed, 32)
+    lat = synth.make_latent(s2, 1, args.seed + 2)
+    slot = synth.make_cache_slot(s2, 1, args.seed)
+    cache = dict(K=slot["K"][:, 0], V=slot["V"][:, 0], H=slot["H"][:, 0])
+    w0 = time.perf_counter()
+    O.reuse_step(s2, W, lat[0], 842, 789, text_kv(s2, W, args.seed + 2), idx2, cache, lat[0], dt=f32)
+    t_r = time.perf_counter() - w0
+    del slot, cache
+    sd, Wd, nd = first_blocks(s2, 4)
+    tkv = text_kv(sd, Wd, args.seed + 2)
+    w0 = time.perf_counter()
+    O.dense_step(sd, Wd, lat[0], 842, 789, tkv, dt=f32)
+    t_d = (time.perf_counter() - w0) * L / nd
+    out["512px"] = dict(tokens=s2.tokens, active=int(len(idx2)), reuse_step_s=round(t_r, 3), dense_step_s=round(t_d, 3),
+                        sample=f"region step: all {L} blocks; dense step: first {nd} blocks, time x {L}/{nd}")
+    # 1024 px dense step
+    s3, W3, n3 = first_blocks(shape, 1)
+    lat = synth.make_latent(shape, 1, args.seed)
+    tkv = text_kv(s3, W3, args.seed)
+    w0 = time.perf_counter()
+    O.dense_step(s3, W3, lat[0], 842, 789, tkv, dt=f32)
+    t_d3 = (time.perf_counter() - w0) * L / n3
+    out["1024px_dense"] = dict(tokens=shape.tokens, dense_step_s=round(t_d3, 3),
+                               sample=f"first {n3} of {L} blocks, time x {L}/{n3}")
+    # localisation read-out at 1024 px
+    nl = 4
+    Z, delta, blob = synth.make_logits(nl, 16, 4096, 120, 64, 64, n_delta=6, seed=args.seed, frac=0.12)
+    w0 = time.perf_counter()
+    maps = O.maps_from_logits(Z, delta, dt=f32)
+    t_m = (time.perf_counter() - w0) * 28 / nl
+    w0 = time.perf_counter()
+    O.localize(maps, 64, 64, theta=0.3, radius=1)
+    t_l = time.perf_counter() - w0
+    out["localize_1024px"] = dict(maps_s=round(t_m, 3), mask_and_compaction_s=round(t_l, 3),
+                                  sample=f"logits [{nl},16,4096,120] as float32, maps time x 28/{nl}; 6 delta columns")
+    log("oracle (float32) on the other workloads: " + json.dumps(out))
+    return out
 
 
 if __name__ == "__main__":
