@@ -313,6 +313,14 @@ def main():
         "resolution_sweep": res,
         "hosted_pool": hosted,
         "cpu_baseline": cpu,
+        # the paper's own figures (one RTX L20, trained PixArt-alpha on editing
+        # datasets, precision unstated): context for the speedups above, not a target
+        "paper_context": {"hardware": "one NVIDIA RTX L20 (Sec. 4.1), precision not stated",
+                          "end_to_end_speedup_range": [1.43, 2.55],
+                          "table2_speedup": {"total": 1.57, "self_attention": 2.89},
+                          "fig9_self_attention_speedup": {"512px": 2.7, "1024px": 4.7, "2048px": ">6"},
+                          "comparable_here": ["schedule.speedup_vs_all_dense", "speedup_vs_dense",
+                                              "resolution_sweep.*.speedup"]},
     }
     print(json.dumps(out), flush=True)
 
